@@ -1,0 +1,262 @@
+"""Seeded synthetic inputs for the SONIC segment-attention path.
+
+This module is shared, as *input only*, by the fp64 oracle (``oracle/``) and by
+the HIP path (``paper_2601_21927_amd``).  It holds none of the method's
+arithmetic: it draws token layouts (roles and segment ids in the order of the
+augmented sequence of Eq.(1), Sec. 3.1) and bf16 Q/K/V bit patterns, nothing
+else.  Neither the mask rules nor attention nor compaction appear here.
+
+Role codes follow the token classes named in Sec. 3.1-3.2: system prompt,
+history body text, Nexus token, current query.
+
+Recipe (fixed draw order, numpy PCG64 seeded with the workload number):
+structure -> per-head scales -> Q -> K -> V -> per-step decode q, k, v.
+fp32 samples are rounded to bf16 by round-to-nearest-even and handed over as
+raw uint16 bit patterns, so both sides read identical bits.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+ROLE_SYSTEM = 0
+ROLE_HISTORY_TEXT = 1
+ROLE_NEXUS = 2
+ROLE_CURRENT = 3
+
+
+# ---------------------------------------------------------------------------
+# bf16 encoding (input encoding only)
+# ---------------------------------------------------------------------------
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bf16 (round-to-nearest-even), return uint16 bits."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32).astype(np.uint64)
+    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return rounded.astype(np.uint16)
+
+
+# ---------------------------------------------------------------------------
+# layouts
+# ---------------------------------------------------------------------------
+@dataclasses.dataclass
+class RequestLayout:
+    """One request of the augmented sequence {I_sys, m_1, N^(1), ..., m_h, N^(h), Q_curr}."""
+    system: int
+    bodies: List[int]
+    nexus: List[int]
+    current: int
+
+    @property
+    def length(self) -> int:
+        return self.system + sum(self.bodies) + sum(self.nexus) + self.current
+
+    def roles_and_turns(self, first_turn: int = 1):
+        """Per-token role codes and segment ids (segment i of the history gets id first_turn+i)."""
+        role = np.empty(self.length, dtype=np.uint8)
+        turn = np.empty(self.length, dtype=np.int32)
+        p = 0
+        role[p:p + self.system] = ROLE_SYSTEM
+        turn[p:p + self.system] = 0
+        p += self.system
+        for i, (b, k) in enumerate(zip(self.bodies, self.nexus)):
+            role[p:p + b] = ROLE_HISTORY_TEXT
+            turn[p:p + b] = first_turn + i
+            p += b
+            role[p:p + k] = ROLE_NEXUS
+            turn[p:p + k] = first_turn + i
+            p += k
+        role[p:p + self.current] = ROLE_CURRENT
+        turn[p:p + self.current] = first_turn + len(self.bodies)
+        p += self.current
+        assert p == self.length
+        return role, turn
+
+
+@dataclasses.dataclass
+class Batch:
+    """A packed (varlen) batch: token-major tensors, request b at rows cu[b]:cu[b+1]."""
+    name: str
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    layouts: List[RequestLayout]
+    role: np.ndarray            # uint8 [T]
+    turn_id: np.ndarray         # int32 [T]
+    cu_seqlens: np.ndarray      # int32 [B+1]
+    q: Optional[np.ndarray] = None   # uint16 bf16 bits [T, Hq, d]
+    k: Optional[np.ndarray] = None   # uint16 bf16 bits [T, Hkv, d]
+    v: Optional[np.ndarray] = None   # uint16 bf16 bits [T, Hkv, d]
+    decode_steps: int = 0
+    dec_q: Optional[np.ndarray] = None   # uint16 [steps, B, Hq, d]
+    dec_k: Optional[np.ndarray] = None   # uint16 [steps, B, Hkv, d]
+    dec_v: Optional[np.ndarray] = None   # uint16 [steps, B, Hkv, d]
+    scale_q: Optional[np.ndarray] = None
+    scale_k: Optional[np.ndarray] = None
+    scale_v: Optional[np.ndarray] = None
+
+    @property
+    def batch(self) -> int:
+        return len(self.layouts)
+
+    @property
+    def total_tokens(self) -> int:
+        return int(self.cu_seqlens[-1])
+
+    @property
+    def max_seqlen(self) -> int:
+        if self.batch == 0:
+            return 0
+        return int(np.max(np.diff(self.cu_seqlens)))
+
+
+def pack_layouts(layouts: Sequence[RequestLayout]):
+    roles, turns, cu = [], [], [0]
+    for lay in layouts:
+        r, t = lay.roles_and_turns()
+        roles.append(r)
+        turns.append(t)
+        cu.append(cu[-1] + lay.length)
+    role = np.concatenate(roles) if roles else np.zeros(0, np.uint8)
+    turn = np.concatenate(turns) if turns else np.zeros(0, np.int32)
+    return role.astype(np.uint8), turn.astype(np.int32), np.asarray(cu, dtype=np.int32)
+
+
+def _normal_bf16(rng: np.random.Generator, shape, scale=None) -> np.ndarray:
+    x = rng.standard_normal(size=shape, dtype=np.float32)
+    if scale is not None:
+        x *= scale.astype(np.float32)
+    return f32_to_bf16_bits(x)
+
+
+def _draw_tensors(rng, batch: Batch, scales: bool, decode_steps: int):
+    T, Hq, Hkv, d = batch.total_tokens, batch.num_q_heads, batch.num_kv_heads, batch.head_dim
+    sq = sk = sv = None
+    if scales:
+        sq = rng.uniform(0.5, 2.0, size=Hq)
+        sk = rng.uniform(0.5, 2.0, size=Hkv)
+        sv = rng.uniform(0.5, 2.0, size=Hkv)
+        batch.scale_q, batch.scale_k, batch.scale_v = sq, sk, sv
+    sqb = None if sq is None else sq[None, :, None]
+    skb = None if sk is None else sk[None, :, None]
+    svb = None if sv is None else sv[None, :, None]
+    batch.q = _normal_bf16(rng, (T, Hq, d), sqb)
+    batch.k = _normal_bf16(rng, (T, Hkv, d), skb)
+    batch.v = _normal_bf16(rng, (T, Hkv, d), svb)
+    B = batch.batch
+    batch.decode_steps = decode_steps
+    if decode_steps:
+        batch.dec_q = _normal_bf16(rng, (decode_steps, B, Hq, d), None if sq is None else sq[None, None, :, None])
+        batch.dec_k = _normal_bf16(rng, (decode_steps, B, Hkv, d), None if sk is None else sk[None, None, :, None])
+        batch.dec_v = _normal_bf16(rng, (decode_steps, B, Hkv, d), None if sv is None else sv[None, None, :, None])
+
+
+def make_batch(name, layouts, Hq, Hkv, d, seed, decode_steps=0, scales=False, tensors=True) -> Batch:
+    role, turn, cu = pack_layouts(layouts)
+    b = Batch(name=name, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=d, layouts=list(layouts),
+              role=role, turn_id=turn, cu_seqlens=cu)
+    if tensors:
+        rng = np.random.default_rng(seed)
+        _draw_tensors(rng, b, scales, decode_steps)
+    return b
+
+
+# ---------------------------------------------------------------------------
+# the five workloads
+# ---------------------------------------------------------------------------
+WORKLOADS = {
+    1: "tiny: B=1, 4/2 heads, d=64, S=32, 3 x (128 text + 8 Nexus), C=64, 16 decode steps",
+    2: "llama3-8b-shape: B=8, 32/8 heads, d=128, S=256, 8 x (512 text + 102 Nexus), C=256, 256 decode steps",
+    3: "ragged-50pct: B=16, 32/8 heads, d=128, h~U{2..12}, b~U{64..1024}, k=b/2, S~U{128..512}, "
+       "C~U{32..512}, per-head scales U[0.5,2], 256 decode steps",
+    4: "long-dialogue: B=4, 28/4 heads, d=128, S=512, 32 x (1024 text + 204 Nexus), C=512, 512 decode steps",
+    5: "dynamic-budget decode: B=64, 32/8 heads, d=128, full context U{1024..8192}, budget {10,20,50}%, "
+       "1024 decode steps",
+}
+
+
+def _uniform_layouts(n, S, b, k, h, C):
+    return [RequestLayout(S, [b] * h, [k] * h, C) for _ in range(n)]
+
+
+def workload_structure(index: int) -> dict:
+    """Layouts and head shapes of a workload, drawn first from its seeded generator."""
+    rng = np.random.default_rng(index)
+    if index == 1:
+        return dict(layouts=_uniform_layouts(1, 32, 128, 8, 3, 64), Hq=4, Hkv=2, d=64, steps=16, scales=False)
+    if index == 2:
+        return dict(layouts=_uniform_layouts(8, 256, 512, 102, 8, 256), Hq=32, Hkv=8, d=128, steps=256,
+                    scales=False)
+    if index == 3:
+        lays = []
+        for _ in range(16):
+            h = int(rng.integers(2, 13))
+            S = int(rng.integers(128, 513))
+            bodies = [int(x) for x in rng.integers(64, 1025, size=h)]
+            nexus = [b // 2 for b in bodies]
+            C = int(rng.integers(32, 513))
+            lays.append(RequestLayout(S, bodies, nexus, C))
+        return dict(layouts=lays, Hq=32, Hkv=8, d=128, steps=256, scales=True, rng=rng)
+    if index == 4:
+        return dict(layouts=_uniform_layouts(4, 512, 1024, 204, 32, 512), Hq=28, Hkv=4, d=128, steps=512,
+                    scales=False)
+    if index == 5:
+        lays, ratios, full = [], [], []
+        for _ in range(64):
+            L_full = int(rng.integers(1024, 8193))
+            r = float(rng.choice([0.1, 0.2, 0.5]))
+            S = int(rng.integers(64, 257))
+            C = int(rng.integers(32, 257))
+            hist = L_full - S - C
+            bodies = []
+            while hist > 0:
+                b = int(rng.integers(64, 1025))
+                if b >= hist:
+                    b = hist
+                bodies.append(b)
+                hist -= b
+            if len(bodies) > 1 and bodies[-1] < 64:
+                tail = bodies.pop()
+                bodies[-1] += tail
+            nexus = [max(1, int(np.floor(r * b))) for b in bodies]
+            lays.append(RequestLayout(S, bodies, nexus, C))
+            ratios.append(r)
+            full.append(L_full)
+        return dict(layouts=lays, Hq=32, Hkv=8, d=128, steps=1024, scales=False, ratios=ratios,
+                    full_lengths=full, rng=rng)
+    raise ValueError(f"unknown workload {index}")
+
+
+def workload(index: int, tensors: bool = True, decode_steps: Optional[int] = None) -> Batch:
+    """Build workload `index` (1..5).  The structure draw precedes the tensor draws on one stream."""
+    st = workload_structure(index)
+    # structures drawn from the stream continue on it; uniform ones draw nothing first
+    rng = st["rng"] if "rng" in st else np.random.default_rng(index)
+    role, turn, cu = pack_layouts(st["layouts"])
+    b = Batch(name=f"workload{index}", num_q_heads=st["Hq"], num_kv_heads=st["Hkv"], head_dim=st["d"],
+              layouts=st["layouts"], role=role, turn_id=turn, cu_seqlens=cu)
+    steps = st["steps"] if decode_steps is None else decode_steps
+    b.decode_steps = steps
+    if tensors:
+        _draw_tensors(rng, b, st["scales"], steps)
+    if index == 5:
+        b.ratios = st["ratios"]
+        b.full_lengths = st["full_lengths"]
+    return b
+
+
+def random_layout(rng: np.random.Generator, max_h=4, max_b=80, max_k=40, max_s=70, max_c=70,
+                  allow_empty_body=False) -> RequestLayout:
+    """A random well-formed layout for property tests (any part may be empty except bodies)."""
+    h = int(rng.integers(0, max_h + 1))
+    lo = 0 if allow_empty_body else 1
+    bodies = [int(x) for x in rng.integers(lo if lo else 1, max_b + 1, size=h)]
+    nexus = [int(x) for x in rng.integers(0, max_k + 1, size=h)]
+    return RequestLayout(int(rng.integers(0, max_s + 1)), bodies, nexus, int(rng.integers(0, max_c + 1)))
+
+
+def text_only_layout(lay: RequestLayout) -> RequestLayout:
+    """The same conversation without Nexus tokens: what a full-context model keeps."""
+    return RequestLayout(lay.system, list(lay.bodies), [0] * len(lay.bodies), lay.current)
