@@ -1,0 +1,209 @@
+/*
+ * sonic.h - C ABI of the SONIC segment-structured attention path on MI355X (gfx950).
+ *
+ * SONIC (Segmented Optimized Nexus for Information Compression) inserts Nexus
+ * tokens after every history segment of a multi-turn conversation, restricts
+ * attention with a hierarchical visibility mask, then keeps only the system
+ * prompt, the Nexus tokens and the current query in the KV cache.  This
+ * library runs the three steps of that path on one GPU:
+ *
+ *   sonic_segment_attn_prefill  - attention over the augmented sequence of
+ *                                 Eq.(1) under the mask of Sec. 3.2, Eqs.(3)-(5);
+ *   sonic_kv_compact            - the KV retention rule (Sec. 3, Fig. 2 caption;
+ *                                 Sec. 3.2 after Eq.(4); App. C);
+ *   sonic_compressed_decode     - one generation step over the retained context
+ *                                 {I_sys, N, Q_n} (App. C, Eq.(15)).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers marked "device" are HIP device pointers; "host" pointers are CPU
+ *   memory.  The caller owns every buffer.  The three GPU calls never allocate,
+ *   free or synchronise: all work is enqueued on `stream` (a hipStream_t; NULL is
+ *   the default stream).
+ * - Tensors are token-major and packed over the batch ("varlen"): request b owns
+ *   rows cu_seqlens[b] .. cu_seqlens[b+1]-1.  Q is bf16 [T][Hq][d]; K and V are
+ *   bf16 [T][Hkv][d]; outputs are fp32 [T][Hq][d].  bf16 values are passed as
+ *   raw 16-bit patterns.  Rows are contiguous (no strides).
+ * - Grouped-query attention: q-head h reads kv-head h / (Hq / Hkv).
+ * - Roles (one byte per token): SONIC_ROLE_*.  turn_id is the history segment
+ *   index: constant within a segment (its body and its Nexus tokens), strictly
+ *   increasing from one history segment to the next, ignored for system and
+ *   current tokens.  A request must read
+ *       SYSTEM* ( HISTORY_TEXT+ NEXUS* )* CURRENT*
+ *   (Eq.(1)); anything else is a layout error.  A segment may have zero Nexus
+ *   tokens; it then ends at its last body token.
+ * - Synchronous errors (bad arguments, unsupported shapes, small workspace) are
+ *   returned before anything is enqueued; outputs are untouched.
+ * - Asynchronous errors (layout grammar, cache capacity) are found by the
+ *   kernels and written to the device word *dev_status (first error wins).  The
+ *   caller zeroes *dev_status before first use.  While it is non-zero every
+ *   later kernel of this library that receives it returns without writing its
+ *   outputs, so an error is sticky until the caller clears it.
+ * - Setting the environment variable SONIC_DEBUG_SYNC=1 makes each GPU call
+ *   synchronise its stream and return the device status (debugging only).
+ * - Thread safety: calls are independent; the library keeps no mutable global
+ *   state apart from a per-device cache of launch parameters.
+ */
+#ifndef SONIC_H
+#define SONIC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    SONIC_OK = 0,
+    SONIC_ERR_INVALID_ARG = 1,   /* null pointer, negative or inconsistent size      */
+    SONIC_ERR_BAD_LAYOUT = 2,    /* role / turn_id sequence breaks the Eq.(1) order  */
+    SONIC_ERR_CAPACITY = 3,      /* a request needs more cache rows than it owns     */
+    SONIC_ERR_WORKSPACE = 4,     /* workspace smaller than the *_workspace_bytes()   */
+    SONIC_ERR_UNSUPPORTED = 5,   /* head_dim not in {64,128}, Hq/Hkv > 8, ...        */
+    SONIC_ERR_HIP = 6            /* a HIP runtime call failed                        */
+};
+
+enum {
+    SONIC_ROLE_SYSTEM = 0,       /* I_sys                                            */
+    SONIC_ROLE_HISTORY_TEXT = 1, /* body B_i of a history segment m_i                */
+    SONIC_ROLE_NEXUS = 2,        /* Nexus token of N_i                               */
+    SONIC_ROLE_CURRENT = 3       /* Q_curr, and every generated token                */
+};
+
+/* Version of this ABI (bumped on any signature or layout change). */
+int32_t sonic_abi_version(void);
+
+/* Static text for a status code. */
+const char *sonic_status_string(int32_t status);
+
+/* ------------------------------------------------------------------------ */
+/* Host-side helpers (pure CPU, no GPU needed)                               */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Check the layout grammar of a packed batch (Eq.(1), Sec. 3.1) on the CPU.
+ * cu_seqlens: host [batch+1]; role, turn_id: host [cu_seqlens[batch]].
+ * Returns SONIC_OK or SONIC_ERR_BAD_LAYOUT (then *bad_request, if non-NULL,
+ * receives the first failing request) or SONIC_ERR_INVALID_ARG.
+ */
+int32_t sonic_validate_layout_host(int32_t batch, const int32_t *cu_seqlens, const uint8_t *role,
+                                   const int32_t *turn_id, int32_t *bad_request);
+
+/*
+ * Per-request work figures of a well-formed batch, on the CPU:
+ *   visible_pairs[b] - number of (query, key) pairs the mask of Sec. 3.2 leaves
+ *                      visible; prefill does 4*d flops per pair and q-head;
+ *   kept_rows[b]     - rows retained by compaction (system + Nexus + current).
+ * Either output may be NULL.  Returns SONIC_ERR_BAD_LAYOUT on a grammar error.
+ */
+int32_t sonic_layout_stats_host(int32_t batch, const int32_t *cu_seqlens, const uint8_t *role,
+                                const int32_t *turn_id, int64_t *visible_pairs, int32_t *kept_rows);
+
+/* ------------------------------------------------------------------------ */
+/* Step 1: masked prefill attention                                          */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of device workspace sonic_segment_attn_prefill needs for this batch. */
+size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens);
+
+/*
+ * out[p][h] = sum_q softmax_q(scale * <q[p][h], k[q][g(h)]> + M[p][q]) * v[q][g(h)]
+ * for every token p of every request, where M is the hierarchical visibility
+ * mask of Sec. 3.2: causal (Eq.(3), applied globally), history bodies removed
+ * for every position after their segment's last Nexus token (Eq.(4)), and all
+ * Nexus tokens mutually visible within and across segments (Eq.(5)).
+ * Fully masked key blocks are never visited: the kernels enumerate the visible
+ * keys of each block of query rows from the segment structure.
+ *
+ *   batch, total_tokens   B and T = cu_seqlens[B] (host values)
+ *   num_q_heads/kv_heads  Hq, Hkv; Hq % Hkv == 0 and Hq / Hkv <= 8
+ *   head_dim              d in {64, 128}
+ *   cu_seqlens            device int32 [B+1], non-decreasing, cu[0] = 0
+ *   role, turn_id         device uint8 [T], int32 [T]
+ *   q                     device bf16 [T][Hq][d];  k, v: device bf16 [T][Hkv][d]
+ *   softmax_scale         e.g. 1/sqrt(d)
+ *   out                   device fp32 [T][Hq][d] (fully written on success)
+ *   workspace             device, >= sonic_prefill_workspace_bytes(B, T) bytes,
+ *                         256-byte aligned; contents need no initialisation
+ *   dev_status            device int32 (see conventions); SONIC_ERR_BAD_LAYOUT
+ *                         is reported here and then no output is written
+ */
+int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t num_q_heads,
+                                   int32_t num_kv_heads, int32_t head_dim, const int32_t *cu_seqlens,
+                                   const uint8_t *role, const int32_t *turn_id, const void *q, const void *k,
+                                   const void *v, float softmax_scale, float *out, void *workspace,
+                                   size_t workspace_bytes, int32_t *dev_status, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Step 2: KV compaction                                                     */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Keep the K/V rows of every token whose role is not HISTORY_TEXT, in order
+ * (system prompt, Nexus tokens, current query; Sec. 3, Fig. 2 caption).
+ * Request b's j-th kept token goes to cache row cache_row_off[b] + j, bit for
+ * bit; keep_idx at that row receives its request-local source position; and
+ * cache_len[b] receives the kept count.  Rows from the kept count up to the
+ * request's capacity are not written.
+ *
+ *   batch, total_tokens, max_seqlen  host values; max_seqlen >= every request length
+ *   num_kv_heads, head_dim           Hkv, d (d in {64, 128})
+ *   cu_seqlens, role                 device, as for the prefill
+ *   k, v                             device bf16 [T][Hkv][d]
+ *   k_cache, v_cache                 device bf16 [rows][Hkv][d]
+ *   cache_row_off                    device int64 [B]: first cache row of request b
+ *   cache_row_cap                    device int32 [B]: rows request b owns
+ *   cache_len                        device int32 [B], written
+ *   keep_idx                         device int32 [rows], written at kept rows
+ *   dev_status                       device int32; SONIC_ERR_CAPACITY when a
+ *                                    request keeps more rows than its capacity
+ *                                    (no row beyond the capacity is written)
+ */
+int32_t sonic_kv_compact(int32_t batch, int32_t total_tokens, int32_t max_seqlen, int32_t num_kv_heads,
+                         int32_t head_dim, const int32_t *cu_seqlens, const uint8_t *role, const void *k,
+                         const void *v, void *k_cache, void *v_cache, const int64_t *cache_row_off,
+                         const int32_t *cache_row_cap, int32_t *cache_len, int32_t *keep_idx,
+                         int32_t *dev_status, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Step 3: decode over the compacted cache                                   */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of device workspace sonic_compressed_decode needs. */
+size_t sonic_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t head_dim, int32_t max_ctx);
+
+/*
+ * One generation step for every request b (App. C, Eq.(15)): the new token's
+ * k_new[b], v_new[b] are appended at cache row cache_row_off[b] + cache_len[b],
+ * then
+ *     out[b][h] = softmax(scale * q[b][h] . Kc^T) Vc
+ * over the request's rows 0 .. cache_len[b] (the appended row included): a
+ * generated token belongs to the current turn, so it sees every retained row.
+ * cache_len[b] is incremented on the device, so a decode loop needs no host
+ * round trip.
+ *
+ * With row_role == NULL the cache is a compact one and every row is visible.
+ * With row_role != NULL (device uint8 [rows], indexed like cache rows) the
+ * cache is a full, uncompacted one: rows whose role is HISTORY_TEXT are masked
+ * (Eq.(4)); the caller marks rows appended by earlier steps as CURRENT.
+ *
+ *   max_ctx        host bound: cache_len[b] + 1 <= max_ctx for every b
+ *   q              device bf16 [B][Hq][d];  k_new, v_new: device bf16 [B][Hkv][d]
+ *   out            device fp32 [B][Hq][d]
+ *   workspace      device, >= sonic_decode_workspace_bytes(B, Hq, d, max_ctx)
+ *   dev_status     SONIC_ERR_CAPACITY when cache_len[b] + 1 exceeds the
+ *                  capacity or max_ctx; that request is then left unchanged
+ */
+int32_t sonic_compressed_decode(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                int32_t max_ctx, void *k_cache, void *v_cache, const int64_t *cache_row_off,
+                                const int32_t *cache_row_cap, int32_t *cache_len, const uint8_t *row_role,
+                                const void *q, const void *k_new, const void *v_new, float softmax_scale,
+                                float *out, void *workspace, size_t workspace_bytes, int32_t *dev_status,
+                                void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SONIC_H */

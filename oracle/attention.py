@@ -58,10 +58,9 @@ def request_probs(q, k, role, turn_id, h: int, scale=None, rows=None) -> np.ndar
 def prefill_request(q, k, v, role, turn_id, scale=None, rows=None, block=512,
                     parsed: Parsed = None) -> np.ndarray:
     """O[rows, Hq, d] for one request: dense scores, explicit mask, softmax, P @ V."""
-    qf = bf16_bits_to_f64(q)
     kf = bf16_bits_to_f64(k)
     vf = bf16_bits_to_f64(v)
-    L, Hq, d = qf.shape
+    L, Hq, d = q.shape
     Hkv = kf.shape[1]
     if Hq % Hkv:
         raise ValueError("num_q_heads must be a multiple of num_kv_heads")
@@ -73,10 +72,11 @@ def prefill_request(q, k, v, role, turn_id, scale=None, rows=None, block=512,
     out = np.zeros((len(rows), Hq, d), dtype=np.float64)
     for r0 in range(0, len(rows), block):
         rb = rows[r0:r0 + block]
+        qf = bf16_bits_to_f64(q[rb])          # only the query rows of this block
         vis = visibility_rows(role, turn_id, rb, parsed=parsed)
         for h in range(Hq):
             g = kv_head(h, Hq, Hkv)
-            scores = scale * (qf[rb, h, :] @ kf[:, g, :].T)
+            scores = scale * (qf[:, h, :] @ kf[:, g, :].T)
             probs = softmax_probs(scores, vis)
             out[r0:r0 + len(rb), h, :] = probs @ vf[:, g, :]
     return out

@@ -1,0 +1,326 @@
+// C ABI entry points: argument checks, workspace carving and kernel launches.
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "common.h"
+
+namespace sonic {
+hipError_t launch_plan(int batch, int total_tokens, const int32_t *cu, const uint8_t *role, const int32_t *turn,
+                       PrefillWs ws, int32_t *status, hipStream_t stream);
+hipError_t prefill_occupancy(int D, int G, int *blocks);
+hipError_t launch_prefill(int D, int G, int grid, const int32_t *cu, const uint16_t *q, const uint16_t *k,
+                          const uint16_t *v, float *out, PrefillWs ws, int Hkv, float scale_log2, hipStream_t stream);
+hipError_t launch_compact(int batch, int total_tokens, int max_seqlen, int Hkv, int D, const int32_t *cu,
+                          const uint8_t *role,
+                          const uint16_t *k, const uint16_t *v, uint16_t *kc, uint16_t *vc, const int64_t *row_off,
+                          const int32_t *row_cap, int32_t *cache_len, int32_t *keep_idx, int32_t *status,
+                          hipStream_t stream);
+int decode_num_splits(int max_ctx, int rows_per_split);
+hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int rows_per_split, uint16_t *kc,
+                         uint16_t *vc, const int64_t *row_off, const int32_t *row_cap, int32_t *cache_len,
+                         const uint8_t *row_role, const uint16_t *q, const uint16_t *k_new, const uint16_t *v_new,
+                         float scale_log2, float *out, float *ws, int32_t *status, hipStream_t stream);
+
+namespace {
+
+constexpr int kAbiVersion = 1;
+constexpr double kLog2e = 1.4426950408889634;
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool debug_sync() {
+  static const bool on = [] {
+    const char *e = std::getenv("SONIC_DEBUG_SYNC");
+    return e != nullptr && e[0] == '1';
+  }();
+  return on;
+}
+
+// Device facts needed for launch shapes, cached per device.
+struct DeviceInfo {
+  bool valid = false;
+  int num_cus = 0;
+  int prefill_blocks[2][9] = {};   // [D == 128][G]: resident workgroups per CU
+};
+
+std::mutex g_dev_mutex;
+std::vector<DeviceInfo> g_dev;
+
+hipError_t device_info(DeviceInfo **out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(g_dev_mutex);
+  if (static_cast<int>(g_dev.size()) <= dev) g_dev.resize(dev + 1);
+  DeviceInfo &d = g_dev[dev];
+  if (!d.valid) {
+    e = hipDeviceGetAttribute(&d.num_cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    for (int di = 0; di < 2; ++di)
+      for (int G = 1; G <= 8; ++G) {
+        int blocks = 0;
+        e = prefill_occupancy(di ? 128 : 64, G, &blocks);
+        if (e != hipSuccess) return e;
+        d.prefill_blocks[di][G] = blocks > 0 ? blocks : 1;
+      }
+    d.valid = true;
+  }
+  *out = &d;
+  return hipSuccess;
+}
+
+int32_t finish(hipError_t e, int32_t *dev_status, hipStream_t stream) {
+  if (e != hipSuccess) return SONIC_ERR_HIP;
+  if (debug_sync()) {
+    if (hipStreamSynchronize(stream) != hipSuccess) return SONIC_ERR_HIP;
+    int32_t st = 0;
+    if (hipMemcpy(&st, dev_status, sizeof(st), hipMemcpyDeviceToHost) != hipSuccess) return SONIC_ERR_HIP;
+    return st;
+  }
+  return SONIC_OK;
+}
+
+// ---------------------------------------------------------------- host grammar
+struct HostSeg {
+  int body_start, body_len, nexus_len;
+};
+struct HostParsed {
+  int length = 0, system = 0, current = 0;
+  std::vector<HostSeg> segs;
+};
+
+// Split one request per Eq.(1): SYSTEM* (TEXT+ NEXUS*)* CURRENT*, segment ids
+// constant within a segment and strictly increasing across segments.
+bool host_parse(const uint8_t *role, const int32_t *turn, int L, HostParsed *out) {
+  out->length = L;
+  out->segs.clear();
+  int p = 0;
+  while (p < L && role[p] == kSystem) ++p;
+  out->system = p;
+  bool have_prev = false;
+  int prev_turn = 0;
+  while (p < L && role[p] == kText) {
+    const int t = turn[p];
+    if (have_prev && t <= prev_turn) return false;
+    const int b0 = p;
+    while (p < L && role[p] == kText && turn[p] == t) ++p;
+    const int n0 = p;
+    while (p < L && role[p] == kNexus) {
+      if (turn[p] != t) return false;
+      ++p;
+    }
+    out->segs.push_back(HostSeg{b0, n0 - b0, p - n0});
+    have_prev = true;
+    prev_turn = t;
+  }
+  const int c0 = p;
+  while (p < L && role[p] == kCurrent) ++p;
+  if (p != L) return false;
+  out->current = L - c0;
+  return true;
+}
+
+}  // namespace
+}  // namespace sonic
+
+using namespace sonic;
+
+extern "C" {
+
+int32_t sonic_abi_version(void) { return kAbiVersion; }
+
+const char *sonic_status_string(int32_t s) {
+  switch (s) {
+    case SONIC_OK: return "ok";
+    case SONIC_ERR_INVALID_ARG: return "invalid argument";
+    case SONIC_ERR_BAD_LAYOUT: return "role/turn_id layout breaks the augmented-sequence order";
+    case SONIC_ERR_CAPACITY: return "cache capacity exceeded";
+    case SONIC_ERR_WORKSPACE: return "workspace too small";
+    case SONIC_ERR_UNSUPPORTED: return "unsupported shape";
+    case SONIC_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int32_t sonic_validate_layout_host(int32_t batch, const int32_t *cu, const uint8_t *role, const int32_t *turn_id,
+                                   int32_t *bad_request) {
+  if (batch < 0 || cu == nullptr || (batch > 0 && cu[batch] > 0 && (role == nullptr || turn_id == nullptr)))
+    return SONIC_ERR_INVALID_ARG;
+  if (cu[0] != 0) return SONIC_ERR_INVALID_ARG;
+  HostParsed hp;
+  for (int b = 0; b < batch; ++b) {
+    if (cu[b + 1] < cu[b]) return SONIC_ERR_INVALID_ARG;
+    if (!host_parse(role + cu[b], turn_id + cu[b], cu[b + 1] - cu[b], &hp)) {
+      if (bad_request) *bad_request = b;
+      return SONIC_ERR_BAD_LAYOUT;
+    }
+  }
+  return SONIC_OK;
+}
+
+int32_t sonic_layout_stats_host(int32_t batch, const int32_t *cu, const uint8_t *role, const int32_t *turn_id,
+                                int64_t *visible_pairs, int32_t *kept_rows) {
+  int32_t bad = -1;
+  const int32_t st = sonic_validate_layout_host(batch, cu, role, turn_id, &bad);
+  if (st != SONIC_OK) return st;
+  HostParsed hp;
+  for (int b = 0; b < batch; ++b) {
+    host_parse(role + cu[b], turn_id + cu[b], cu[b + 1] - cu[b], &hp);
+    const int64_t S = hp.system, C = hp.current;
+    int64_t k_tot = 0;
+    for (const HostSeg &s : hp.segs) k_tot += s.nexus_len;
+    // system rows: causal; body row r of segment i: S + (Nexus before i) + r + 1;
+    // Nexus row of segment i: S + b_i + K_tot; current row r: S + K_tot + r + 1.
+    int64_t pairs = S * (S + 1) / 2 + C * (S + k_tot) + C * (C + 1) / 2;
+    int64_t before = 0;
+    for (const HostSeg &s : hp.segs) {
+      const int64_t bl = s.body_len, kl = s.nexus_len;
+      pairs += bl * (S + before) + bl * (bl + 1) / 2 + kl * (S + bl + k_tot);
+      before += kl;
+    }
+    if (visible_pairs) visible_pairs[b] = pairs;
+    if (kept_rows) kept_rows[b] = static_cast<int32_t>(S + k_tot + C);
+  }
+  return SONIC_OK;
+}
+
+// ---------------------------------------------------------------- prefill
+static size_t prefill_ws_layout(int32_t batch, int32_t T, PrefillWs *ws, char *base) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes, 256);
+    return base ? base + o : nullptr;
+  };
+  char *req = take(sizeof(ReqInfo) * static_cast<size_t>(batch > 0 ? batch : 1));
+  char *npos = take(sizeof(int32_t) * static_cast<size_t>(T > 0 ? T : 1));
+  char *runs = take(sizeof(int2) * static_cast<size_t>(T > 0 ? T : 1));
+  char *tiles = take(sizeof(TileDesc) * static_cast<size_t>(T > 0 ? T : 1));
+  char *order = take(sizeof(int32_t) * static_cast<size_t>(T > 0 ? T : 1));
+  char *ctrl = take(sizeof(int32_t) * 16);
+  if (ws) {
+    ws->req = reinterpret_cast<ReqInfo *>(req);
+    ws->nexus_pos = reinterpret_cast<int32_t *>(npos);
+    ws->runs = reinterpret_cast<int2 *>(runs);
+    ws->tiles = reinterpret_cast<TileDesc *>(tiles);
+    ws->order = reinterpret_cast<int32_t *>(order);
+    ws->ctrl = reinterpret_cast<int32_t *>(ctrl);
+  }
+  return off;
+}
+
+size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens) {
+  if (batch < 0 || total_tokens < 0) return 0;
+  return prefill_ws_layout(batch, total_tokens, nullptr, nullptr);
+}
+
+int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t Hq, int32_t Hkv, int32_t d,
+                                   const int32_t *cu_seqlens, const uint8_t *role, const int32_t *turn_id,
+                                   const void *q, const void *k, const void *v, float softmax_scale, float *out,
+                                   void *workspace, size_t workspace_bytes, int32_t *dev_status, void *stream_) {
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  if (batch < 0 || total_tokens < 0 || Hq <= 0 || Hkv <= 0 || dev_status == nullptr) return SONIC_ERR_INVALID_ARG;
+  if (d != 64 && d != 128) return SONIC_ERR_UNSUPPORTED;
+  if (Hq % Hkv != 0) return SONIC_ERR_INVALID_ARG;
+  const int G = Hq / Hkv;
+  if (G > 8) return SONIC_ERR_UNSUPPORTED;
+  if (!std::isfinite(softmax_scale)) return SONIC_ERR_INVALID_ARG;
+  if (batch == 0 || total_tokens == 0) return SONIC_OK;
+  if (!cu_seqlens || !role || !turn_id || !q || !k || !v || !out || !workspace) return SONIC_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) || !aligned(workspace, 256))
+    return SONIC_ERR_INVALID_ARG;
+  if (static_cast<size_t>(total_tokens) * Hq * d >= (size_t(1) << 40)) return SONIC_ERR_UNSUPPORTED;
+  PrefillWs ws;
+  const size_t need = prefill_ws_layout(batch, total_tokens, &ws, static_cast<char *>(workspace));
+  if (workspace_bytes < need) return SONIC_ERR_WORKSPACE;
+  DeviceInfo *di = nullptr;
+  hipError_t e = device_info(&di);
+  if (e != hipSuccess) return SONIC_ERR_HIP;
+  e = launch_plan(batch, total_tokens, cu_seqlens, role, turn_id, ws, dev_status, stream);
+  if (e != hipSuccess) return SONIC_ERR_HIP;
+  int grid = di->num_cus * di->prefill_blocks[d == 128][G];
+  grid = (grid + kNumXcd - 1) / kNumXcd * kNumXcd;
+  e = launch_prefill(d, G, grid, cu_seqlens, static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k),
+                     static_cast<const uint16_t *>(v), out, ws, Hkv, static_cast<float>(softmax_scale * kLog2e),
+                     stream);
+  return finish(e, dev_status, stream);
+}
+
+// ---------------------------------------------------------------- compaction
+int32_t sonic_kv_compact(int32_t batch, int32_t total_tokens, int32_t max_seqlen, int32_t Hkv, int32_t d,
+                         const int32_t *cu_seqlens, const uint8_t *role, const void *k, const void *v, void *k_cache,
+                         void *v_cache, const int64_t *cache_row_off, const int32_t *cache_row_cap,
+                         int32_t *cache_len, int32_t *keep_idx, int32_t *dev_status, void *stream_) {
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  if (batch < 0 || total_tokens < 0 || max_seqlen < 0 || Hkv <= 0 || dev_status == nullptr)
+    return SONIC_ERR_INVALID_ARG;
+  if (batch > 65535) return SONIC_ERR_UNSUPPORTED;
+  if (d != 64 && d != 128) return SONIC_ERR_UNSUPPORTED;
+  if (batch == 0) return SONIC_OK;
+  if (!cu_seqlens || !cache_row_off || !cache_row_cap || !cache_len) return SONIC_ERR_INVALID_ARG;
+  if (total_tokens > 0 && (!role || !k || !v || !k_cache || !v_cache || !keep_idx)) return SONIC_ERR_INVALID_ARG;
+  if (total_tokens > 0 && (!aligned(role, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(k_cache, 16) ||
+                           !aligned(v_cache, 16)))
+    return SONIC_ERR_INVALID_ARG;
+  hipError_t e = launch_compact(batch, total_tokens, max_seqlen, Hkv, d, cu_seqlens, role, static_cast<const uint16_t *>(k),
+                                static_cast<const uint16_t *>(v), static_cast<uint16_t *>(k_cache),
+                                static_cast<uint16_t *>(v_cache), cache_row_off, cache_row_cap, cache_len, keep_idx,
+                                dev_status, stream);
+  return finish(e, dev_status, stream);
+}
+
+// ---------------------------------------------------------------- decode
+static int decode_rows_per_split(int32_t batch, int32_t Hkv, int32_t max_ctx) {
+  // aim for about 2048 workgroups over the whole batch, 64..1024 rows each
+  const long pairs = static_cast<long>(batch) * Hkv;
+  long rows = (static_cast<long>(max_ctx) * pairs + 2047) / 2048;
+  rows = (rows + 63) / 64 * 64;
+  if (rows < 64) rows = 64;
+  if (rows > 1024) rows = 1024;
+  return static_cast<int>(rows);
+}
+
+size_t sonic_decode_workspace_bytes(int32_t batch, int32_t Hq, int32_t d, int32_t max_ctx) {
+  if (batch <= 0 || Hq <= 0 || max_ctx <= 0) return 256;
+  // the split count depends on Hkv only through the heuristic; take the smallest split size
+  const int nsplit = decode_num_splits(max_ctx, 64);
+  return align_up(static_cast<size_t>(batch) * Hq * nsplit * (d + 2) * sizeof(float), 256);
+}
+
+int32_t sonic_compressed_decode(int32_t batch, int32_t Hq, int32_t Hkv, int32_t d, int32_t max_ctx, void *k_cache,
+                                void *v_cache, const int64_t *cache_row_off, const int32_t *cache_row_cap,
+                                int32_t *cache_len, const uint8_t *row_role, const void *q, const void *k_new,
+                                const void *v_new, float softmax_scale, float *out, void *workspace,
+                                size_t workspace_bytes, int32_t *dev_status, void *stream_) {
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  if (batch < 0 || Hq <= 0 || Hkv <= 0 || max_ctx <= 0 || dev_status == nullptr) return SONIC_ERR_INVALID_ARG;
+  if (d != 64 && d != 128) return SONIC_ERR_UNSUPPORTED;
+  if (Hq % Hkv != 0) return SONIC_ERR_INVALID_ARG;
+  if (Hq / Hkv > 8) return SONIC_ERR_UNSUPPORTED;
+  if (batch > 65535 || Hkv > 65535) return SONIC_ERR_UNSUPPORTED;
+  if (!std::isfinite(softmax_scale)) return SONIC_ERR_INVALID_ARG;
+  if (batch == 0) return SONIC_OK;
+  if (!k_cache || !v_cache || !cache_row_off || !cache_row_cap || !cache_len || !q || !k_new || !v_new || !out ||
+      !workspace)
+    return SONIC_ERR_INVALID_ARG;
+  if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(q, 16) || !aligned(k_new, 16) ||
+      !aligned(v_new, 16) || !aligned(out, 16) || !aligned(workspace, 16))
+    return SONIC_ERR_INVALID_ARG;
+  const int rps = decode_rows_per_split(batch, Hkv, max_ctx);
+  const size_t need =
+      static_cast<size_t>(batch) * Hq * decode_num_splits(max_ctx, rps) * (d + 2) * sizeof(float);
+  if (workspace_bytes < need) return SONIC_ERR_WORKSPACE;
+  hipError_t e = launch_decode(batch, Hq, Hkv, d, max_ctx, rps, static_cast<uint16_t *>(k_cache),
+                               static_cast<uint16_t *>(v_cache), cache_row_off, cache_row_cap, cache_len, row_role,
+                               static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k_new),
+                               static_cast<const uint16_t *>(v_new), static_cast<float>(softmax_scale * kLog2e), out,
+                               static_cast<float *>(workspace), dev_status, stream);
+  return finish(e, dev_status, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,88 @@
+// Shared device-side definitions of the SONIC HIP kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/sonic.h"
+
+namespace sonic {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kNumXcd = 8;          // MI355X: 8 accelerator complex dies, one L2 each
+
+// Roles (one byte per token), as in sonic.h.
+constexpr int kSystem = SONIC_ROLE_SYSTEM;
+constexpr int kText = SONIC_ROLE_HISTORY_TEXT;
+constexpr int kNexus = SONIC_ROLE_NEXUS;
+constexpr int kCurrent = SONIC_ROLE_CURRENT;
+
+__device__ __forceinline__ void raise_status(int32_t *status, int32_t code) {
+  atomicCAS(status, 0, code);
+}
+
+// Read the status word once per workgroup so that every wave takes the same
+// early-exit decision (waves must not diverge around a later barrier).
+__device__ __forceinline__ bool block_status_clear(const int32_t *status, int *lds_flag) {
+  if (threadIdx.x == 0) *lds_flag = (__atomic_load_n(status, __ATOMIC_RELAXED) == 0) ? 1 : 0;
+  __syncthreads();
+  return *lds_flag != 0;
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Prefill work descriptor of one block of up to 32 query rows that share one
+// visible-key list.  The keys are taken, in this order, from
+//   [0, r0_end)                      contiguous, every row sees them
+//   nexus_pos[0, nx)                 gathered Nexus positions, every row sees them
+//   [r1_start, r1_start + r1_len)    contiguous, every row sees them
+//   [p0, p0 + ndiag)                 the block's own rows, causal (key j seen by row >= j)
+// All positions are request-local.
+struct TileDesc {
+  int32_t req;
+  int32_t p0;
+  int32_t nrows;
+  int32_t r0_end;
+  int32_t nx;
+  int32_t r1_start;
+  int32_t r1_len;
+  int32_t ndiag;
+};
+static_assert(sizeof(TileDesc) == 32, "descriptor is eight words");
+
+constexpr int kTileRows = 32;       // query rows per descriptor (one MFMA N block)
+constexpr int kKeyChunk = 64;       // keys per inner-loop step
+
+__host__ __device__ __forceinline__ int tile_key_count(const TileDesc &t) {
+  return t.r0_end + t.nx + t.r1_len + t.ndiag;
+}
+__host__ __device__ __forceinline__ int tile_cost(const TileDesc &t) {
+  return (tile_key_count(t) + kKeyChunk - 1) / kKeyChunk;
+}
+
+// Per-request summary written by the planner.
+struct ReqInfo {
+  int32_t ntiles;
+  int32_t system;
+  int32_t nexus_total;
+  int32_t nruns;
+};
+
+// Device workspace of the prefill, carved from one caller buffer.
+struct PrefillWs {
+  ReqInfo *req;        // [B]
+  int32_t *nexus_pos;  // [T]  request b's Nexus positions at offset cu[b]
+  int2 *runs;          // [T]  (run start, Nexus count before it) at offset cu[b]
+  TileDesc *tiles;     // [T]  request b's descriptors at offset cu[b]
+  int32_t *order;      // [T]  descriptor slots, most expensive first
+  int32_t *ctrl;       // [16] ctrl[0] = number of descriptors, ctrl[8 + x] = queue head of XCD x
+};
+
+}  // namespace sonic

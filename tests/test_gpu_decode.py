@@ -1,0 +1,164 @@
+"""Decode over the compacted cache on the GPU against the fp64 oracle."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import decode as OD
+from paper_2601_21927_amd import sonic
+from paper_2601_21927_amd.runner import bf16_to_device, bf16_to_host
+from tests import gpu_helpers as H
+
+pytestmark = pytest.mark.gpu
+
+
+def compacted(batch, extra_rows):
+    """Compact the batch on the GPU (its bit-exactness is tested elsewhere) and check it here too."""
+    db = H.device_batch(batch)
+    kept = H.kept_counts(batch)
+    cache = db.alloc_cache(kept + extra_rows)
+    assert db.compact() == sonic.OK
+    torch.cuda.synchronize()
+    assert db.read_status() == 0
+    kc, vc, ki, n, off = H.oracle_compact(batch, kept + extra_rows)
+    assert np.array_equal(cache.length.cpu().numpy(), n)
+    return db, cache, (kc, vc, n, off)
+
+
+def run_steps(batch, db, cache, steps, check_steps, row_role=None, oracle_ctx=None):
+    """Run `steps` decode steps; compare the outputs of `check_steps` with the oracle.
+    oracle_ctx(b, t) -> (k_ctx, v_ctx) bits for request b before step t."""
+    B, Hq, d = batch.batch, batch.num_q_heads, batch.head_dim
+    max_ctx = int(cache.row_cap_host.max())
+    out = torch.empty((B, Hq, d), dtype=torch.float32, device="cuda")
+    qs = bf16_to_device(batch.dec_q[:steps])
+    ks = bf16_to_device(batch.dec_k[:steps])
+    vs = bf16_to_device(batch.dec_v[:steps])
+    errs = []
+    for t in range(steps):
+        st = cache.decode(qs[t], ks[t], vs[t], out, db.status, max_ctx, row_role=row_role)
+        assert st == sonic.OK, sonic.status_string(st)
+        if t in check_steps:
+            torch.cuda.synchronize()
+            assert db.read_status() == 0, sonic.status_string(db.read_status())
+            got = out.cpu().numpy()
+            for b in range(B):
+                kc, vc = oracle_ctx(b, t)
+                want = OD.decode_step(batch.dec_q[t, b], kc, vc, batch.dec_k[t, b], batch.dec_v[t, b])
+                errs.append(np.abs(got[b] - want))
+                H.assert_close(got[b], want, f"{batch.name} step {t} request {b}")
+    torch.cuda.synchronize()
+    return np.concatenate([e.ravel() for e in errs]) if errs else np.zeros(0)
+
+
+def compact_ctx_fn(batch, ref):
+    kc, vc, n, off = ref
+
+    def ctx(b, t):
+        base, ln = int(off[b]), int(n[b])
+        k = np.concatenate([kc[base:base + ln], batch.dec_k[:t, b]])
+        v = np.concatenate([vc[base:base + ln], batch.dec_v[:t, b]])
+        return k, v
+    return ctx
+
+
+@pytest.mark.parametrize("Hq,Hkv,d", [(4, 2, 64), (32, 8, 128), (28, 4, 128), (8, 8, 128), (8, 1, 64)])
+def test_decode_random_layouts(Hq, Hkv, d):
+    H.need_gpu()
+    rng = np.random.default_rng(200 + Hq + Hkv + d)
+    lays = [W.random_layout(rng, max_h=4, max_b=400, max_k=150, max_s=300, max_c=200) for _ in range(5)]
+    lays.append(W.RequestLayout(0, [], [], 1))     # a context of one row
+    steps = 6
+    batch = W.make_batch("rand", lays, Hq, Hkv, d, seed=int(rng.integers(1 << 30)), decode_steps=steps)
+    db, cache, ref = compacted(batch, steps)
+    run_steps(batch, db, cache, steps, set(range(steps)), oracle_ctx=compact_ctx_fn(batch, ref))
+    # lengths advanced on the device and appended rows are in the cache, bit for bit
+    kc, vc, n, off = ref
+    assert np.array_equal(cache.length.cpu().numpy(), n + steps)
+    k = bf16_to_host(cache.k)
+    for b in range(batch.batch):
+        base = int(off[b]) + int(n[b])
+        assert np.array_equal(k[base:base + steps], batch.dec_k[:steps, b])
+
+
+def test_masked_full_cache_decode_equals_compact():
+    """Full-cache mode (history rows masked by role) against the oracle's masked decode."""
+    H.need_gpu()
+    rng = np.random.default_rng(77)
+    lays = [W.random_layout(rng, max_h=4, max_b=300, max_k=100, max_s=200, max_c=100) for _ in range(4)]
+    steps = 4
+    batch = W.make_batch("full", lays, 32, 8, 128, seed=77, decode_steps=steps)
+    db = H.device_batch(batch)
+    # the full cache is the uncompacted augmented K/V, with room for the steps
+    lens = np.array([l.length for l in lays], np.int64)
+    cache = db.alloc_cache(lens + steps)
+    kf = bf16_to_host(cache.k)
+    vf = bf16_to_host(cache.v)
+    roles = np.full(int((lens + steps).sum()), sonic.ROLE_CURRENT, np.uint8)
+    for b in range(batch.batch):
+        s, e = int(batch.cu_seqlens[b]), int(batch.cu_seqlens[b + 1])
+        o = int(cache.row_off_host[b])
+        kf[o:o + e - s] = batch.k[s:e]
+        vf[o:o + e - s] = batch.v[s:e]
+        roles[o:o + e - s] = batch.role[s:e]
+    cache.k.copy_(bf16_to_device(kf))
+    cache.v.copy_(bf16_to_device(vf))
+    cache.length.copy_(torch.from_numpy(lens.astype(np.int32)))
+    row_role = torch.from_numpy(roles).cuda()
+
+    def ctx_masked(b, t):
+        raise AssertionError("unused")
+
+    B, Hq, d = batch.batch, batch.num_q_heads, batch.head_dim
+    out = torch.empty((B, Hq, d), dtype=torch.float32, device="cuda")
+    max_ctx = int(cache.row_cap_host.max())
+    for t in range(steps):
+        st = cache.decode(bf16_to_device(batch.dec_q[t]), bf16_to_device(batch.dec_k[t]),
+                          bf16_to_device(batch.dec_v[t]), out, db.status, max_ctx, row_role=row_role)
+        assert st == sonic.OK
+        torch.cuda.synchronize()
+        assert db.read_status() == 0
+        got = out.cpu().numpy()
+        for b in range(B):
+            s, e = int(batch.cu_seqlens[b]), int(batch.cu_seqlens[b + 1])
+            kfull = np.concatenate([batch.k[s:e], batch.dec_k[:t, b]])
+            vfull = np.concatenate([batch.v[s:e], batch.dec_v[:t, b]])
+            rfull = np.concatenate([batch.role[s:e], np.full(t, sonic.ROLE_CURRENT, np.uint8)])
+            want = OD.masked_decode_step(batch.dec_q[t, b], kfull, vfull, rfull, batch.dec_k[t, b],
+                                         batch.dec_v[t, b])
+            H.assert_close(got[b], want, f"masked full decode step {t} request {b}")
+
+
+@pytest.mark.parametrize("idx,check", [(1, None), (2, (0, 1, 100, 255)), (3, (0, 255)), (4, (0, 511)),
+                                       (5, (0, 1, 1023))])
+def test_decode_workloads(idx, check):
+    H.need_gpu()
+    batch = W.workload(idx)
+    steps = batch.decode_steps
+    check = set(range(steps)) if check is None else set(check)
+    H.note(f"decode workload {idx}: B={batch.batch} steps={steps}")
+    db, cache, ref = compacted(batch, steps)
+    errs = run_steps(batch, db, cache, steps, check, oracle_ctx=compact_ctx_fn(batch, ref))
+    H.note(f"  workload {idx} decode overall: max_abs={errs.max():.3e} mean_abs={errs.mean():.3e}")
+    kc, vc, n, off = ref
+    assert np.array_equal(cache.length.cpu().numpy(), n + steps)
+
+
+def test_decode_capacity_overflow():
+    H.need_gpu()
+    lays = [W.RequestLayout(4, [10], [3], 2), W.RequestLayout(2, [5], [1], 1)]
+    batch = W.make_batch("cap", lays, 4, 2, 64, seed=3, decode_steps=3)
+    db, cache, ref = compacted(batch, np.array([1, 3]))
+    out = torch.full((2, 4, 64), 5.0, dtype=torch.float32, device="cuda")
+    max_ctx = int(cache.row_cap_host.max())
+    q, kn, vn = (bf16_to_device(x) for x in (batch.dec_q, batch.dec_k, batch.dec_v))
+    assert cache.decode(q[0], kn[0], vn[0], out, db.status, max_ctx) == sonic.OK
+    torch.cuda.synchronize()
+    assert db.read_status() == 0
+    lens = cache.length.cpu().numpy().copy()
+    out.fill_(5.0)
+    assert cache.decode(q[1], kn[1], vn[1], out, db.status, max_ctx) == sonic.OK   # request 0 is full now
+    torch.cuda.synchronize()
+    assert db.read_status() == sonic.ERR_CAPACITY
+    assert np.array_equal(cache.length.cpu().numpy(), lens)
+    assert torch.all(out == 5.0)

@@ -9,14 +9,17 @@ else.  Neither the mask rules nor attention nor compaction appear here.
 Role codes follow the token classes named in Sec. 3.1-3.2: system prompt,
 history body text, Nexus token, current query.
 
-Recipe (fixed draw order, numpy PCG64 seeded with the workload number):
-structure -> per-head scales -> Q -> K -> V -> per-step decode q, k, v.
-fp32 samples are rounded to bf16 by round-to-nearest-even and handed over as
-raw uint16 bit patterns, so both sides read identical bits.
+Recipe: the structure (and per-head scales) is drawn first from
+numpy PCG64 seeded with the workload number; then each tensor (Q, K, V, per-step
+decode q, k, v) is drawn as N(0,1) float32 in blocks of 2^22 values, block j of
+tensor t from PCG64(SeedSequence([seed, t, j])).  fp32 samples are rounded to
+bf16 by round-to-nearest-even and handed over as raw uint16 bit patterns, so
+both sides read identical bits.
 """
 from __future__ import annotations
 
 import dataclasses
+import os
 from typing import List, Optional, Sequence
 
 import numpy as np
@@ -33,9 +36,13 @@ ROLE_CURRENT = 3
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round float32 values to bf16 (round-to-nearest-even), return uint16 bits."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    return rounded.astype(np.uint16)
+    u = x.view(np.uint32)
+    # finite inputs only (the generators draw normals): the sum cannot wrap in 32 bits
+    r = (u >> 16) & np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r >>= 16
+    return r.astype(np.uint16)
 
 
 # ---------------------------------------------------------------------------
@@ -124,14 +131,41 @@ def pack_layouts(layouts: Sequence[RequestLayout]):
     return role.astype(np.uint8), turn.astype(np.int32), np.asarray(cu, dtype=np.int32)
 
 
-def _normal_bf16(rng: np.random.Generator, shape, scale=None) -> np.ndarray:
-    x = rng.standard_normal(size=shape, dtype=np.float32)
-    if scale is not None:
-        x *= scale.astype(np.float32)
-    return f32_to_bf16_bits(x)
+_BLOCK = 1 << 22   # values per independent generator block
 
 
-def _draw_tensors(rng, batch: Batch, scales: bool, decode_steps: int):
+def _normal_bf16(seed, tensor_id: int, shape, scale=None) -> np.ndarray:
+    """N(0,1) (times an optional broadcast scale) rounded to bf16, drawn block by block:
+    block j of tensor `tensor_id` comes from PCG64(SeedSequence([seed, tensor_id, j])), so the
+    bytes do not depend on how many threads fill the blocks."""
+    shape = tuple(int(x) for x in shape)
+    n = int(np.prod(shape)) if shape else 1
+    out = np.empty(n, dtype=np.uint16)
+    sc = None if scale is None else np.broadcast_to(np.asarray(scale, np.float32), shape).reshape(-1)
+
+    def fill(j):
+        a, e = j * _BLOCK, min(n, (j + 1) * _BLOCK)
+        g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([int(seed), int(tensor_id), j])))
+        x = g.standard_normal(e - a, dtype=np.float32)
+        if sc is not None:
+            x *= sc[a:e]
+        out[a:e] = f32_to_bf16_bits(x)
+
+    nblocks = (n + _BLOCK - 1) // _BLOCK
+    if nblocks <= 1:
+        for j in range(nblocks):
+            fill(j)
+    else:
+        import concurrent.futures
+        workers = min(nblocks, max(1, min(16, os.cpu_count() or 1)))
+        with concurrent.futures.ThreadPoolExecutor(max_workers=workers) as ex:
+            list(ex.map(fill, range(nblocks)))
+    return out.reshape(shape)
+
+
+def _draw_tensors(rng, batch: Batch, scales: bool, decode_steps: int, seed: int, with_q: bool = True):
+    """Per-head scales come from the structure stream `rng`; the tensors from per-block streams
+    keyed by `seed` and a fixed tensor id (1 Q, 2 K, 3 V, 4 decode q, 5 decode k, 6 decode v)."""
     T, Hq, Hkv, d = batch.total_tokens, batch.num_q_heads, batch.num_kv_heads, batch.head_dim
     sq = sk = sv = None
     if scales:
@@ -139,18 +173,17 @@ def _draw_tensors(rng, batch: Batch, scales: bool, decode_steps: int):
         sk = rng.uniform(0.5, 2.0, size=Hkv)
         sv = rng.uniform(0.5, 2.0, size=Hkv)
         batch.scale_q, batch.scale_k, batch.scale_v = sq, sk, sv
-    sqb = None if sq is None else sq[None, :, None]
-    skb = None if sk is None else sk[None, :, None]
-    svb = None if sv is None else sv[None, :, None]
-    batch.q = _normal_bf16(rng, (T, Hq, d), sqb)
-    batch.k = _normal_bf16(rng, (T, Hkv, d), skb)
-    batch.v = _normal_bf16(rng, (T, Hkv, d), svb)
+    hs = lambda s: None if s is None else s[:, None]
+    if with_q:
+        batch.q = _normal_bf16(seed, 1, (T, Hq, d), hs(sq))
+    batch.k = _normal_bf16(seed, 2, (T, Hkv, d), hs(sk))
+    batch.v = _normal_bf16(seed, 3, (T, Hkv, d), hs(sv))
     B = batch.batch
     batch.decode_steps = decode_steps
     if decode_steps:
-        batch.dec_q = _normal_bf16(rng, (decode_steps, B, Hq, d), None if sq is None else sq[None, None, :, None])
-        batch.dec_k = _normal_bf16(rng, (decode_steps, B, Hkv, d), None if sk is None else sk[None, None, :, None])
-        batch.dec_v = _normal_bf16(rng, (decode_steps, B, Hkv, d), None if sv is None else sv[None, None, :, None])
+        batch.dec_q = _normal_bf16(seed, 4, (decode_steps, B, Hq, d), hs(sq))
+        batch.dec_k = _normal_bf16(seed, 5, (decode_steps, B, Hkv, d), hs(sk))
+        batch.dec_v = _normal_bf16(seed, 6, (decode_steps, B, Hkv, d), hs(sv))
 
 
 def make_batch(name, layouts, Hq, Hkv, d, seed, decode_steps=0, scales=False, tensors=True) -> Batch:
@@ -159,7 +192,7 @@ def make_batch(name, layouts, Hq, Hkv, d, seed, decode_steps=0, scales=False, te
               role=role, turn_id=turn, cu_seqlens=cu)
     if tensors:
         rng = np.random.default_rng(seed)
-        _draw_tensors(rng, b, scales, decode_steps)
+        _draw_tensors(rng, b, scales, decode_steps, seed)
     return b
 
 
@@ -240,7 +273,8 @@ def workload(index: int, tensors: bool = True, decode_steps: Optional[int] = Non
     steps = st["steps"] if decode_steps is None else decode_steps
     b.decode_steps = steps
     if tensors:
-        _draw_tensors(rng, b, st["scales"], steps)
+        # the dynamic-budget workload is decode-only: its caches come from K/V, it needs no prefill Q
+        _draw_tensors(rng, b, st["scales"], steps, index, with_q=(index != 5))
     if index == 5:
         b.ratios = st["ratios"]
         b.full_lengths = st["full_lengths"]
