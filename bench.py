@@ -1,0 +1,306 @@
+"""Benchmark of the SONIC hot path on one MI355X.
+
+One step = the whole path over one batch of the Llama-3-8B-shaped workload
+(B=8, 32/8 heads, d=128, 256 system + 8 x (512 text + 102 Nexus) + 256 current
+tokens per request): masked prefill, KV compaction, then 256 decode steps
+over the compacted cache.  Inputs are synthetic (seeded bf16 N(0,1)) and
+resident in HBM before the timed region.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline] [--no-graph]
+
+Prints one JSON line.  value = generated tokens per second of the whole step
+(B x 256 decode tokens / step time, the step including its prefill and
+compaction).  Per-phase figures, the roofline of the dominant kernel and the
+fp64 CPU oracle's rate on a bounded sample of the same work are attached.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import glob
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "masked-prefill visible TFLOP/s; compressed-decode tok/s; % of MFMA/HBM peak"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2601_21927_amd", "csrc", "*"))):
+        h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch from the committed rocprofv3 counter runs, if they were taken
+    on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    data = json.load(open(path))
+    ent = data.get(kernel)
+    if not ent or ent.get("source_hash") != kernel_source_hash():
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying a HIP graph")
+    ap.add_argument("--decode-steps", type=int, default=256)
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    import workloads as W
+    from paper_2601_21927_amd import sonic
+    from paper_2601_21927_amd.runner import SonicBatch, CompactCache, bf16_to_device
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    sonic.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    batch = W.workload(2, decode_steps=args.decode_steps)
+    B, Hq, Hkv, d = batch.batch, batch.num_q_heads, batch.num_kv_heads, batch.head_dim
+    steps_dec = batch.decode_steps
+    vis_pairs, kept = sonic.layout_stats_host(batch.cu_seqlens, batch.role, batch.turn_id)
+    visible_flops = float(4 * d * Hq * vis_pairs.sum())
+
+    db = SonicBatch(batch.role, batch.turn_id, batch.cu_seqlens, batch.q, batch.k, batch.v, device=dev)
+    caps = kept.astype(np.int64) + steps_dec
+    cache = db.alloc_cache(caps)
+    max_ctx = int(caps.max())
+    dq = bf16_to_device(batch.dec_q, dev)
+    dk = bf16_to_device(batch.dec_k, dev)
+    dv = bf16_to_device(batch.dec_v, dev)
+    dec_out = torch.empty((B, Hq, d), dtype=torch.float32, device=dev)
+    # allocate the decode workspace outside the timed region
+    assert cache.decode(dq[0], dk[0], dv[0], dec_out, db.status, max_ctx) == sonic.OK
+    torch.cuda.synchronize()
+
+    # full-context baseline: the same conversations without Nexus tokens, every row visible
+    text_lays = [W.text_only_layout(l) for l in batch.layouts]
+    full_rows = np.array([l.length for l in text_lays], np.int64)
+    full = CompactCache(int((full_rows + steps_dec).sum()), Hkv, d,
+                        np.concatenate([[0], np.cumsum(full_rows + steps_dec)[:-1]]),
+                        (full_rows + steps_dec).astype(np.int32), dev)
+    keep_text = batch.role != W.ROLE_NEXUS
+    kt, vt = batch.k[keep_text], batch.v[keep_text]
+    fk = np.zeros((full.rows, Hkv, d), np.uint16)
+    fv = np.zeros_like(fk)
+    src = 0
+    for b in range(B):
+        o, n = int(full.row_off_host[b]), int(full_rows[b])
+        fk[o:o + n], fv[o:o + n] = kt[src:src + n], vt[src:src + n]
+        src += n
+    full.k.copy_(bf16_to_device(fk, dev))
+    full.v.copy_(bf16_to_device(fv, dev))
+    full_len0 = torch.from_numpy(full_rows.astype(np.int32)).to(dev)
+    full.length.copy_(full_len0)
+    assert full.decode(dq[0], dk[0], dv[0], dec_out, db.status, int(full.row_cap_host.max())) == sonic.OK
+    torch.cuda.synchronize()
+    del fk, fv, kt, vt
+
+    stream = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def run_prefill():
+        st = db.prefill()
+        assert st == sonic.OK, sonic.status_string(st)
+
+    def run_compact():
+        st = db.compact()
+        assert st == sonic.OK, sonic.status_string(st)
+
+    full_max_ctx = int(full.row_cap_host.max())
+
+    def run_decode_loop(c: CompactCache):
+        mc = max_ctx if c is cache else full_max_ctx
+        for t in range(steps_dec):
+            st = c.decode(dq[t], dk[t], dv[t], dec_out, db.status, mc)
+            assert st == sonic.OK, sonic.status_string(st)
+
+    phases = {"prefill": run_prefill, "compact": run_compact, "decode": lambda: run_decode_loop(cache)}
+    for _ in range(max(1, args.warmup)):
+        for f in phases.values():
+            f()
+    torch.cuda.synchronize()
+    use_graph = not args.no_graph
+    graphs = {}
+    if use_graph:
+        # one HIP graph per phase; a step replays the three in order
+        for name, f in phases.items():
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                f()
+            graphs[name] = g
+        torch.cuda.synchronize()
+        full_graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(full_graph):
+            run_decode_loop(full)
+        torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+
+    def step(marks=None):
+        for i, name in enumerate(("prefill", "compact", "decode")):
+            if marks: marks[i].record(stream)
+            if use_graph:
+                graphs[name].replay()
+            else:
+                phases[name]()
+        if marks: marks[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    assert db.read_status() == 0, sonic.status_string(db.read_status())
+
+    # ---- timed region: exactly K steps ----
+    all_marks = [[ev() for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(all_marks[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    assert db.read_status() == 0, sonic.status_string(db.read_status())
+    ms_per_step = wall * 1e3 / args.steps
+    med = lambda i, j: float(np.median([m[i].elapsed_time(m[j]) for m in all_marks]))
+    pf_ms, cp_ms, dc_ms = med(0, 1), med(1, 2), med(2, 3)
+    step_ms_ev = med(0, 3)
+
+    # ---- full-context decode (same kernel, text-only cache) for the speedup ----
+    fms = []
+    for _ in range(3):
+        full.length.copy_(full_len0)
+        a, b_ = ev(), ev()
+        a.record(stream)
+        if use_graph:
+            full_graph.replay()
+        else:
+            run_decode_loop(full)
+        b_.record(stream)
+        torch.cuda.synchronize()
+        fms.append(a.elapsed_time(b_))
+    full_ms = float(np.median(fms))
+    assert db.read_status() == 0
+
+    # ---- algorithmic work ----
+    row_bytes = Hkv * d * 2                       # one token's K (or V) over all kv-heads, bf16
+    compact_bytes = float(kept.sum()) * row_bytes * 2 * 2 + batch.total_tokens + float(kept.sum()) * 4
+    ctx = kept[None, :].astype(np.float64) + np.arange(1, steps_dec + 1)[:, None]   # rows read per step
+    decode_bytes = float(ctx.sum()) * row_bytes * 2
+    full_ctx = full_rows[None, :].astype(np.float64) + np.arange(1, steps_dec + 1)[:, None]
+    full_bytes = float(full_ctx.sum()) * row_bytes * 2
+
+    prefill_tflops = visible_flops / (pf_ms * 1e-3) / 1e12
+    compact_gbs = compact_bytes / (cp_ms * 1e-3) / 1e9
+    decode_gbs = decode_bytes / (dc_ms * 1e-3) / 1e9
+    decode_tok_s = B * steps_dec / (dc_ms * 1e-3)
+    value = B * steps_dec / (ms_per_step * 1e-3)
+
+    shares = {"prefill": pf_ms, "compact": cp_ms, "decode": dc_ms}
+    dominant = max(shares, key=shares.get)
+    if dominant == "prefill":
+        roof = {"bound": "mfma", "achieved": round(prefill_tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(prefill_tflops / PEAK_BF16_TFLOPS, 4),
+                "traffic": measured_traffic("prefill_kernel"), "kernel": "prefill (plan + prefill_kernel)"}
+    elif dominant == "decode":
+        per_launch = decode_bytes / steps_dec
+        ach = per_launch / (dc_ms * 1e-3 / steps_dec) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": measured_traffic("decode_split_kernel"),
+                "kernel": "decode step (decode_split_kernel + decode_combine_kernel)"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(compact_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(compact_gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic("compact_kernel"),
+                "kernel": "compact_kernel"}
+
+    rec = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tok/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "llama3-8b-shape: B=8, Hq/Hkv=32/8, d=128, S=256, 8 x (512 text + 102 Nexus), "
+                               "C=256, L=5424, 256 decode steps", "global_batch": B, "seq_len": int(batch.max_seqlen),
+                   "parallelism": "single-gpu", "graph": use_graph},
+        "phases": {
+            "prefill_ms": round(pf_ms, 4), "prefill_visible_tflops": round(prefill_tflops, 2),
+            "prefill_frac_bf16_peak": round(prefill_tflops / PEAK_BF16_TFLOPS, 4),
+            "compact_us": round(cp_ms * 1e3, 2), "compact_gbs": round(compact_gbs, 1),
+            "compact_frac_hbm_peak": round(compact_gbs / PEAK_HBM_GBS, 4),
+            "decode_ms_256_steps": round(dc_ms, 4), "decode_us_per_step": round(dc_ms * 1e3 / steps_dec, 2),
+            "decode_tok_s": round(decode_tok_s, 1), "decode_gbs": round(decode_gbs, 1),
+            "decode_frac_hbm_peak": round(decode_gbs / PEAK_HBM_GBS, 4),
+            "full_context_decode_ms": round(full_ms, 4), "full_context_decode_gbs": round(full_bytes / (full_ms * 1e-3) / 1e9, 1),
+            "decode_speedup_vs_full_context": round(full_ms / dc_ms, 3),
+            "step_ms_event_median": round(step_ms_ev, 4),
+        },
+        "work": {"visible_flops": visible_flops, "compact_bytes": compact_bytes, "decode_bytes": decode_bytes,
+                 "full_decode_bytes": full_bytes},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(batch, kept)
+    print(json.dumps(rec), flush=True)
+
+
+def cpu_baseline(batch, kept):
+    """The fp64 oracle, as it stands, on a bounded sample of one step; scaled to tok/s."""
+    import threading  # noqa: F401
+    from oracle import attention as OA
+    from oracle import compaction as OC
+    from oracle import decode as OD
+    cores = len(os.sched_getaffinity(0))
+    cu = batch.cu_seqlens
+    B = batch.batch
+    steps = batch.decode_steps
+    # prefill: 96 query rows of request 0, scaled to all rows of the batch
+    s, e = int(cu[0]), int(cu[1])
+    rows = np.linspace(0, e - s - 1, 96).astype(np.int64)
+    t0 = time.perf_counter()
+    OA.prefill_request(batch.q[s:e], batch.k[s:e], batch.v[s:e], batch.role[s:e], batch.turn_id[s:e], rows=rows)
+    t_pre = (time.perf_counter() - t0) * batch.total_tokens / len(rows)
+    # compaction: request 0, scaled to the batch
+    caps = kept.astype(np.int64)
+    kc = np.zeros((int(caps[0]), batch.num_kv_heads, batch.head_dim), np.uint16)
+    t0 = time.perf_counter()
+    OC.compact_batch(batch.k[s:e], batch.v[s:e], batch.role[s:e], np.array([0, e - s]), [0], [caps[0]], kc,
+                     kc.copy(), np.zeros(int(caps[0]), np.int32))
+    t_cmp = (time.perf_counter() - t0) * B
+    # decode: 4 steps of request 0 (at the mean context of the loop), scaled to B x steps
+    t0 = time.perf_counter()
+    mid = steps // 2
+    kctx = np.concatenate([kc, batch.dec_k[:mid, 0]])
+    for t in range(4):
+        OD.decode_step(batch.dec_q[mid + t, 0], kctx, kctx, batch.dec_k[mid + t, 0], batch.dec_v[mid + t, 0])
+    t_dec = (time.perf_counter() - t0) / 4 * B * steps
+    total = t_pre + t_cmp + t_dec
+    return {"value": round(B * steps / total, 3), "unit": "tok/s", "cores": cores, "kind": "oracle",
+            "sample": f"fp64 oracle: 96 prefill rows of request 0 (scaled to {batch.total_tokens} rows), "
+                      f"compaction of request 0 (scaled x{B}), 4 decode steps of request 0 at mid context "
+                      f"(scaled to {B}x{steps}); estimated step time {total:.1f} s",
+            "prefill_s_est": round(t_pre, 2), "compact_s_est": round(t_cmp, 3), "decode_s_est": round(t_dec, 2)}
+
+
+if __name__ == "__main__":
+    main()

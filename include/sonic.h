@@ -122,7 +122,7 @@ size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens);
  *   cu_seqlens            device int32 [B+1], non-decreasing, cu[0] = 0
  *   role, turn_id         device uint8 [T], int32 [T]
  *   q                     device bf16 [T][Hq][d];  k, v: device bf16 [T][Hkv][d]
- *   softmax_scale         e.g. 1/sqrt(d)
+ *   softmax_scale         finite and > 0, e.g. 1/sqrt(d)
  *   out                   device fp32 [T][Hq][d] (fully written on success)
  *   workspace             device, >= sonic_prefill_workspace_bytes(B, T) bytes,
  *                         256-byte aligned; contents need no initialisation
@@ -170,7 +170,7 @@ int32_t sonic_kv_compact(int32_t batch, int32_t total_tokens, int32_t max_seqlen
 /* Step 3: decode over the compacted cache                                   */
 /* ------------------------------------------------------------------------ */
 
-/* Bytes of device workspace sonic_compressed_decode needs. */
+/* Bytes of device workspace sonic_compressed_decode needs (any Hkv dividing Hq). */
 size_t sonic_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t head_dim, int32_t max_ctx);
 
 /*
@@ -181,7 +181,8 @@ size_t sonic_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t 
  * over the request's rows 0 .. cache_len[b] (the appended row included): a
  * generated token belongs to the current turn, so it sees every retained row.
  * cache_len[b] is incremented on the device, so a decode loop needs no host
- * round trip.
+ * round trip.  Two kernels: split-K partials over the context, then a
+ * log-sum-exp merge that also advances cache_len.
  *
  * With row_role == NULL the cache is a compact one and every row is visible.
  * With row_role != NULL (device uint8 [rows], indexed like cache rows) the
@@ -191,9 +192,13 @@ size_t sonic_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t 
  *   max_ctx        host bound: cache_len[b] + 1 <= max_ctx for every b
  *   q              device bf16 [B][Hq][d];  k_new, v_new: device bf16 [B][Hkv][d]
  *   out            device fp32 [B][Hq][d]
- *   workspace      device, >= sonic_decode_workspace_bytes(B, Hq, d, max_ctx)
- *   dev_status     SONIC_ERR_CAPACITY when cache_len[b] + 1 exceeds the
- *                  capacity or max_ctx; that request is then left unchanged
+ *   workspace      device, 256-byte aligned, >= sonic_decode_workspace_bytes(B, Hq, d,
+ *                  max_ctx); contents need no initialisation
+ *   dev_status     SONIC_ERR_CAPACITY when cache_len[b] + 1 exceeds the capacity
+ *                  or max_ctx: request b is then left unchanged (no append, no
+ *                  output, same length) while the other requests proceed.  Unlike
+ *                  the other calls, decode does not skip work on a pending status.
+ * Calls that share a workspace must not run concurrently.
  */
 int32_t sonic_compressed_decode(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                                 int32_t max_ctx, void *k_cache, void *v_cache, const int64_t *cache_row_off,

@@ -22,7 +22,7 @@ int decode_num_splits(int max_ctx, int rows_per_split);
 hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int rows_per_split, uint16_t *kc,
                          uint16_t *vc, const int64_t *row_off, const int32_t *row_cap, int32_t *cache_len,
                          const uint8_t *row_role, const uint16_t *q, const uint16_t *k_new, const uint16_t *v_new,
-                         float scale_log2, float *out, float *ws, int32_t *status, hipStream_t stream);
+                         float scale_log2, float *out, void *ws, int32_t *status, hipStream_t stream);
 
 namespace {
 
@@ -229,7 +229,7 @@ int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t 
   if (Hq % Hkv != 0) return SONIC_ERR_INVALID_ARG;
   const int G = Hq / Hkv;
   if (G > 8) return SONIC_ERR_UNSUPPORTED;
-  if (!std::isfinite(softmax_scale)) return SONIC_ERR_INVALID_ARG;
+  if (!std::isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SONIC_ERR_INVALID_ARG;
   if (batch == 0 || total_tokens == 0) return SONIC_OK;
   if (!cu_seqlens || !role || !turn_id || !q || !k || !v || !out || !workspace) return SONIC_ERR_INVALID_ARG;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) || !aligned(workspace, 256))
@@ -276,20 +276,29 @@ int32_t sonic_kv_compact(int32_t batch, int32_t total_tokens, int32_t max_seqlen
 
 // ---------------------------------------------------------------- decode
 static int decode_rows_per_split(int32_t batch, int32_t Hkv, int32_t max_ctx) {
-  // aim for about 2048 workgroups over the whole batch, 64..1024 rows each
+  // about `target` workgroups over the whole batch (fewer, longer splits stream better), 64..4096 rows each
+  static const long target = [] {
+    const char *e = std::getenv("SONIC_DECODE_TARGET_BLOCKS");   // tuning override
+    const long v = e ? std::atol(e) : 0;
+    return v > 0 ? v : 512L;
+  }();
   const long pairs = static_cast<long>(batch) * Hkv;
-  long rows = (static_cast<long>(max_ctx) * pairs + 2047) / 2048;
+  long rows = (static_cast<long>(max_ctx) * pairs + target - 1) / target;
   rows = (rows + 63) / 64 * 64;
   if (rows < 64) rows = 64;
-  if (rows > 1024) rows = 1024;
+  if (rows > 4096) rows = 4096;
   return static_cast<int>(rows);
+}
+
+static size_t decode_ws_bytes(int32_t batch, int32_t Hq, int32_t d, int32_t nsplit) {
+  const size_t counts = align_up(static_cast<size_t>(batch) * sizeof(int32_t), 256);
+  return counts + static_cast<size_t>(batch) * Hq * nsplit * (d + 2) * sizeof(float);
 }
 
 size_t sonic_decode_workspace_bytes(int32_t batch, int32_t Hq, int32_t d, int32_t max_ctx) {
   if (batch <= 0 || Hq <= 0 || max_ctx <= 0) return 256;
-  // the split count depends on Hkv only through the heuristic; take the smallest split size
-  const int nsplit = decode_num_splits(max_ctx, 64);
-  return align_up(static_cast<size_t>(batch) * Hq * nsplit * (d + 2) * sizeof(float), 256);
+  // enough for any kv-head count: the smallest split size bounds the split count
+  return align_up(decode_ws_bytes(batch, Hq, d, decode_num_splits(max_ctx, 64)), 256);
 }
 
 int32_t sonic_compressed_decode(int32_t batch, int32_t Hq, int32_t Hkv, int32_t d, int32_t max_ctx, void *k_cache,
@@ -303,23 +312,21 @@ int32_t sonic_compressed_decode(int32_t batch, int32_t Hq, int32_t Hkv, int32_t 
   if (Hq % Hkv != 0) return SONIC_ERR_INVALID_ARG;
   if (Hq / Hkv > 8) return SONIC_ERR_UNSUPPORTED;
   if (batch > 65535 || Hkv > 65535) return SONIC_ERR_UNSUPPORTED;
-  if (!std::isfinite(softmax_scale)) return SONIC_ERR_INVALID_ARG;
+  if (!std::isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SONIC_ERR_INVALID_ARG;
   if (batch == 0) return SONIC_OK;
   if (!k_cache || !v_cache || !cache_row_off || !cache_row_cap || !cache_len || !q || !k_new || !v_new || !out ||
       !workspace)
     return SONIC_ERR_INVALID_ARG;
   if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(q, 16) || !aligned(k_new, 16) ||
-      !aligned(v_new, 16) || !aligned(out, 16) || !aligned(workspace, 16))
+      !aligned(v_new, 16) || !aligned(out, 16) || !aligned(workspace, 256))
     return SONIC_ERR_INVALID_ARG;
   const int rps = decode_rows_per_split(batch, Hkv, max_ctx);
-  const size_t need =
-      static_cast<size_t>(batch) * Hq * decode_num_splits(max_ctx, rps) * (d + 2) * sizeof(float);
-  if (workspace_bytes < need) return SONIC_ERR_WORKSPACE;
+  if (workspace_bytes < decode_ws_bytes(batch, Hq, d, decode_num_splits(max_ctx, rps))) return SONIC_ERR_WORKSPACE;
   hipError_t e = launch_decode(batch, Hq, Hkv, d, max_ctx, rps, static_cast<uint16_t *>(k_cache),
                                static_cast<uint16_t *>(v_cache), cache_row_off, cache_row_cap, cache_len, row_role,
                                static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k_new),
                                static_cast<const uint16_t *>(v_new), static_cast<float>(softmax_scale * kLog2e), out,
-                               static_cast<float *>(workspace), dev_status, stream);
+                               workspace, dev_status, stream);
   return finish(e, dev_status, stream);
 }
 

@@ -1,7 +1,8 @@
 // KV compaction: keep system, Nexus and current-query rows (Sec. 3, Fig. 2
 // caption; Sec. 3.2 after Eq.(4)), dropping every history body row.
 //
-// Grid: (chunk of 1024 input tokens, request, slice).  Each workgroup
+// Grid: (chunk of 1024 input tokens, request, slice); the slice count is chosen
+// so that the launch has about 2048 workgroups.  Each workgroup
 //   1. counts the kept tokens of its request before its chunk (16-byte role
 //      loads, byte-wise compare, popcount, workgroup sum);
 //   2. ranks the kept tokens of its chunk with wave ballots and an LDS scan
@@ -17,7 +18,7 @@ namespace sonic {
 
 constexpr int kCompactThreads = 256;
 constexpr int kCompactChunk = 1024;   // input tokens per workgroup
-constexpr int kCompactSlices = 4;     // workgroups sharing one chunk's copy
+constexpr int kCompactMaxSlices = 32; // workgroups sharing one chunk's copy (grid z)
 
 // Kept (non-history-text) bytes of one 32-bit word, restricted to byte lanes [lo, hi).
 __device__ __forceinline__ int kept_bytes(uint32_t w, int lo, int hi) {
@@ -105,7 +106,8 @@ __global__ __launch_bounds__(kCompactThreads) void compact_kernel(
     if (n > cap) raise_status(status, SONIC_ERR_CAPACITY);
     else cache_len[b] = n;
   }
-  const int per_slice = (chunk_kept + kCompactSlices - 1) / kCompactSlices;
+  const int slices = gridDim.z;
+  const int per_slice = (chunk_kept + slices - 1) / slices;
   const int j0 = slice * per_slice;
   const int j1 = min(chunk_kept, j0 + per_slice);
   const int room = cap - before;   // ranks >= room would overflow the request's rows
@@ -135,7 +137,9 @@ hipError_t launch_compact(int batch, int total_tokens, int max_seqlen, int Hkv, 
                           const int32_t *row_cap, int32_t *cache_len, int32_t *keep_idx, int32_t *status,
                           hipStream_t stream) {
   const int chunks = max(1, (max_seqlen + kCompactChunk - 1) / kCompactChunk);
-  dim3 grid(chunks, batch, kCompactSlices);
+  const long cb = static_cast<long>(chunks) * batch;
+  const int slices = static_cast<int>(max(1L, min(static_cast<long>(kCompactMaxSlices), (2048 + cb - 1) / cb)));
+  dim3 grid(chunks, batch, slices);
   if (D == 64)
     compact_kernel<64><<<grid, dim3(kCompactThreads), 0, stream>>>(cu, role, k, v, kc, vc, row_off, row_cap,
                                                                    cache_len, keep_idx, status, total_tokens, Hkv);

@@ -1,19 +1,25 @@
 // Decode over the retained context {I_sys, N, Q_n} (App. C, Eq.(15)).
 //
-// decode_split_kernel: grid (split, kv-head, request), 4 waves.  A split owns
-// rows [split*R, split*R + R) of the request's context rows 0..len (row len is
-// the token being generated: it is read from k_new/v_new, and split 0 of each
-// kv-head also writes it into the cache).  Each wave takes 16 rows at a time:
+// decode_kernel: grid (split, kv-head, request), 4 waves.  A
+// split owns rows [split*R, split*R + R) of the request's context rows 0..len
+// (row len is the token being generated: it is read from k_new/v_new, and split 0
+// of each kv-head also appends it to the cache).  Each wave walks 16-row groups,
+// loading the next group's K and V while it works on the current one:
 //   scores    S^T (16 rows x 16 cols) = K . Q^T with v_mfma_f32_16x16x32_bf16;
 //             column c < G is q-head kvh*G + c, the other columns are zero;
-//   softmax   per q-head, online, fp32, exp2 with log2(e) folded in;
-//   values    P . V on the vector ALUs in fp32: lane (d chunk, row quarter)
+//   softmax   per q-head, online, fp32, exp2 with log2(e) folded into the scale;
+//   values    P . V on the vector ALUs in fp32: lane (d chunk, row slot)
 //             accumulates 8 d-values of every q-head of the group.
-// The four waves' partial (max, sum, acc) are merged through LDS and one
-// partial per (request, q-head, split) goes to the workspace.
+// The four waves merge through LDS.  With one split the workgroup writes the
+// output; otherwise it stores its partial (max, sum, acc) for decode_combine.
 //
-// decode_combine_kernel: one workgroup per request merges the splits with the
-// log-sum-exp rule, writes out[b] and then increments cache_len[b].
+// decode_combine_kernel: grid (kv-head, request) merges the splits with the
+// log-sum-exp rule and (kv-head 0) advances cache_len.  Cross-workgroup merging
+// is left to a second kernel on purpose: the L2 caches of the eight XCDs are
+// not coherent with each other, so an in-kernel hand-off needs device-scope
+// fences that write back and invalidate a whole L2, evicting the K/V that
+// other workgroups are streaming; the kernel boundary gives the same
+// visibility for free.
 #include "common.h"
 
 namespace sonic {
@@ -22,94 +28,129 @@ constexpr int kDecThreads = 256;
 constexpr int kDecWaves = kDecThreads / kWave;
 constexpr int kDecRowsPerGroup = 16;
 
-template <int D>
-__global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
+struct DecodeWs {
+  float *part;        // [B*Hkv][nsplit][G*(D+2)] partial (m[G], l[G], acc[G][D]) per split
+  int32_t *nsplit;    // [B] splits used by request b in this step (0: request skipped)
+};
+
+template <int D, int G>
+__global__ __launch_bounds__(kDecThreads, 2) void decode_kernel(
     uint16_t *__restrict__ kc, uint16_t *__restrict__ vc, const int64_t *__restrict__ row_off,
-    const int32_t *__restrict__ row_cap, const int32_t *__restrict__ cache_len, const uint8_t *__restrict__ row_role,
+    const int32_t *__restrict__ row_cap, int32_t *__restrict__ cache_len, const uint8_t *__restrict__ row_role,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k_new, const uint16_t *__restrict__ v_new,
-    float *__restrict__ ws, int32_t *status, int Hq, int Hkv, int rows_per_split, int nsplit_max, int max_ctx,
+    float *__restrict__ out, DecodeWs ws, int32_t *status, int Hkv, int rows_per_split, int nsplit_max, int max_ctx,
     float scale_log2) {
-  constexpr int KS = D / 32;      // k steps of the 16x16x32 product
-  constexpr int DCH = D / 8;      // 8-value d chunks (16 lanes cover D = 128; 8 cover D = 64)
-  constexpr int ROWQ = kWave / DCH;   // rows handled per value-load instruction
+  constexpr int KS = D / 32;            // k steps of the 16x16x32 product
+  constexpr int DCH = D / 8;            // 8-value d chunks per row
+  constexpr int ROWQ = kWave / DCH;     // row slots of the value phase
+  constexpr int VPL = kDecRowsPerGroup / ROWQ;   // V rows per lane per group
+  constexpr int REC = G * (D + 2);      // floats of one partial record
   __shared__ float p_lds[kDecWaves][kDecRowsPerGroup][8];
   __shared__ float corr_lds[kDecWaves][8];
   __shared__ float m_lds[kDecWaves][8];
   __shared__ float l_lds[kDecWaves][8];
-  __shared__ float acc_lds[kDecWaves][8][D];
-  __shared__ int s_ok;
+  __shared__ float acc_lds[kDecWaves][G][D];
 
-  if (!block_status_clear(status, &s_ok)) return;
   const int split = blockIdx.x;
   const int kvh = blockIdx.y;
   const int b = blockIdx.z;
-  const int G = Hq / Hkv;
+  const int Hq = Hkv * G;
   const int len = cache_len[b];
   const int n_ctx = len + 1;
-  if (n_ctx > row_cap[b] || n_ctx > max_ctx) {
-    if (split == 0 && kvh == 0 && threadIdx.x == 0) raise_status(status, SONIC_ERR_CAPACITY);
+  if (n_ctx > row_cap[b] || n_ctx > max_ctx) {   // uniform over the request: no append, no output
+    if (split == 0 && kvh == 0 && threadIdx.x == 0) {
+      raise_status(status, SONIC_ERR_CAPACITY);
+      ws.nsplit[b] = 0;
+    }
     return;
   }
+  const int nsp = (n_ctx + rows_per_split - 1) / rows_per_split;
+  if (split == 0 && kvh == 0 && threadIdx.x == 0) ws.nsplit[b] = nsp;
+  if (split >= nsp) return;
   const int r_begin = split * rows_per_split;
-  if (r_begin >= n_ctx) return;
   const int r_end = min(n_ctx, r_begin + rows_per_split);
   const int64_t base = row_off[b];
   const int wave = threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
-  const size_t row_stride = static_cast<size_t>(Hkv) * D;   // elements per cache row
+  const size_t row_stride = static_cast<size_t>(Hkv) * D;
   const uint16_t *knew = k_new + (static_cast<size_t>(b) * Hkv + kvh) * D;
   const uint16_t *vnew = v_new + (static_cast<size_t>(b) * Hkv + kvh) * D;
+  uint16_t *kbase = kc + static_cast<size_t>(base) * row_stride + static_cast<size_t>(kvh) * D;
+  uint16_t *vbase = vc + static_cast<size_t>(base) * row_stride + static_cast<size_t>(kvh) * D;
 
-  // split 0 appends the new token's k/v at row len of this kv-head
-  if (split == 0 && threadIdx.x < DCH) {
-    const size_t dst = (static_cast<size_t>(base + len)) * row_stride + static_cast<size_t>(kvh) * D + threadIdx.x * 8;
-    *reinterpret_cast<u32x4 *>(kc + dst) = reinterpret_cast<const u32x4 *>(knew)[threadIdx.x];
-    *reinterpret_cast<u32x4 *>(vc + dst) = reinterpret_cast<const u32x4 *>(vnew)[threadIdx.x];
+  if (split == 0 && threadIdx.x < DCH) {   // append the new token at row len
+    const size_t dst = static_cast<size_t>(len) * row_stride + threadIdx.x * 8;
+    *reinterpret_cast<u32x4 *>(kbase + dst) = reinterpret_cast<const u32x4 *>(knew)[threadIdx.x];
+    *reinterpret_cast<u32x4 *>(vbase + dst) = reinterpret_cast<const u32x4 *>(vnew)[threadIdx.x];
   }
 
-  // Q^T fragments (B operand of 16x16x32): lane (col = lane%16, quarter = lane/16) holds
+  // Q^T fragments (B operand): lane (col = lane%16, quarter = lane/16) holds
   // d = 32*ks + 8*quarter .. +7 of q-head kvh*G + col (zero for col >= G).
   const int col = lane & 15;
   const int quarter = lane >> 4;
   bf16x8 qf[KS];
   {
-    const bool ok = col < G;
     const uint16_t *qrow = q + (static_cast<size_t>(b) * Hq + kvh * G + col) * D;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       u32x4 w = {0u, 0u, 0u, 0u};
-      if (ok) w = *reinterpret_cast<const u32x4 *>(qrow + 32 * ks + 8 * quarter);
+      if (col < G) w = *reinterpret_cast<const u32x4 *>(qrow + 32 * ks + 8 * quarter);
       qf[ks] = __builtin_bit_cast(bf16x8, w);
     }
   }
+  const int dc = lane % DCH;   // value phase: d chunk
+  const int rq = lane / DCH;   // value phase: row slot
 
-  // value-phase lane roles: d chunk dc (8 values), row slot rq within a 16-row group
-  const int dc = lane % DCH;
-  const int rq = lane / DCH;
-  float acc[8][8];
+  // Rows below len come from the cache; row len is the new token (its inputs, not the
+  // cache, so no split depends on split 0's append).
+  auto load_k = [&](int r0, u32x4 (&kr)[KS]) {
+    const int r = r0 + (lane & 15);
+    const uint16_t *krow = (r < len) ? kbase + static_cast<size_t>(r) * row_stride : knew;
+    const bool ok = r < r_end;
 #pragma unroll
-  for (int hh = 0; hh < 8; ++hh)
+    for (int ks = 0; ks < KS; ++ks) {
+      kr[ks] = u32x4{0u, 0u, 0u, 0u};
+      if (ok) kr[ks] = *reinterpret_cast<const u32x4 *>(krow + 32 * ks + 8 * quarter);
+    }
+  };
+  auto load_v = [&](int r0, u32x4 (&vr)[VPL]) {
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) {
+      const int r = r0 + rq + i * ROWQ;
+      const uint16_t *vrow = (r < len) ? vbase + static_cast<size_t>(r) * row_stride : vnew;
+      vr[i] = u32x4{0u, 0u, 0u, 0u};
+      if (r < r_end) vr[i] = *reinterpret_cast<const u32x4 *>(vrow + 8 * dc);
+    }
+  };
+
+  float acc[G][8];
+#pragma unroll
+  for (int hh = 0; hh < G; ++hh)
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[hh][e] = 0.f;
-  float m_run = -INFINITY;   // running max of head `col` (score lanes)
-  float l_run = 0.f;         // this lane's share of the running sum of head `col`
+  float m_run = -INFINITY;
+  float l_run = 0.f;
 
-  for (int r0 = r_begin + wave * kDecRowsPerGroup; r0 < r_end; r0 += kDecWaves * kDecRowsPerGroup) {
-    // ---- scores: A operand lane (row = lane%16, quarter) holds d = 32*ks + 8*quarter .. +7 ----
-    f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
-    {
-      const int r = r0 + (lane & 15);
-      const uint16_t *krow = nullptr;
-      if (r < len) krow = kc + static_cast<size_t>(base + r) * row_stride + static_cast<size_t>(kvh) * D;
-      else if (r == len) krow = knew;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        u32x4 w = {0u, 0u, 0u, 0u};
-        if (krow) w = *reinterpret_cast<const u32x4 *>(krow + 32 * ks + 8 * quarter);
-        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), qf[ks], sacc, 0, 0, 0);
-      }
+  constexpr int kStride = kDecWaves * kDecRowsPerGroup;
+  int r0 = r_begin + wave * kDecRowsPerGroup;
+  u32x4 kr[KS], vr[VPL];
+  if (r0 < r_end) {
+    load_k(r0, kr);
+    load_v(r0, vr);
+  }
+  for (; r0 < r_end; r0 += kStride) {
+    // prefetch the next group while this one is processed
+    u32x4 kn[KS], vn[VPL];
+    const int rn = r0 + kStride;
+    if (rn < r_end) {
+      load_k(rn, kn);
+      load_v(rn, vn);
     }
-    // lane (col, quarter) now holds rows r0 + 4*quarter + i, i = 0..3, of head col
+    f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[ks]), qf[ks], sacc, 0, 0, 0);
+    // lane (col, quarter) holds rows r0 + 4*quarter + i, i = 0..3, of head col
     float x[4];
     float mloc = -INFINITY;
 #pragma unroll
@@ -123,7 +164,6 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
     mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
     const float m_new = fmaxf(m_run, mloc);
-    // a group may be fully masked for this head: keep the old max then
     const float corr = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
     float psum = 0.f;
 #pragma unroll
@@ -135,49 +175,48 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
     m_run = m_new;
     l_run = l_run * corr + psum;
     if (quarter == 0 && col < 8) corr_lds[wave][col] = corr;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-    // ---- values: lane (dc, rq) takes rows rq, rq + ROWQ, ... of the group ----
-    float cr[8];
 #pragma unroll
-    for (int hh = 0; hh < 8; ++hh) cr[hh] = corr_lds[wave][hh];
+    for (int hh = 0; hh < G; ++hh) {
+      const float c = corr_lds[wave][hh];
 #pragma unroll
-    for (int hh = 0; hh < 8; ++hh)
+      for (int e = 0; e < 8; ++e) acc[hh][e] *= c;
+    }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[hh][e] *= cr[hh];
-#pragma unroll
-    for (int rr = rq; rr < kDecRowsPerGroup; rr += ROWQ) {
-      const int r = r0 + rr;
-      if (r >= r_end) break;
-      const uint16_t *vrow = (r < len) ? vc + static_cast<size_t>(base + r) * row_stride + static_cast<size_t>(kvh) * D
-                                       : vnew;
-      const u32x4 w = *reinterpret_cast<const u32x4 *>(vrow + 8 * dc);
+    for (int i = 0; i < VPL; ++i) {
+      const int rr = rq + i * ROWQ;
       float vv[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        vv[2 * i] = bf16_lo(w[i]);
-        vv[2 * i + 1] = bf16_hi(w[i]);
+      for (int j = 0; j < 4; ++j) {
+        vv[2 * j] = bf16_lo(vr[i][j]);
+        vv[2 * j + 1] = bf16_hi(vr[i][j]);
       }
 #pragma unroll
-      for (int hh = 0; hh < 8; ++hh) {
-        if (hh < G) {
-          const float p = p_lds[wave][rr][hh];
+      for (int hh = 0; hh < G; ++hh) {
+        const float p = p_lds[wave][rr][hh];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) acc[hh][e] = fmaf(p, vv[e], acc[hh][e]);
-        }
+        for (int e = 0; e < 8; ++e) acc[hh][e] = fmaf(p, vv[e], acc[hh][e]);
       }
     }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kr[ks] = kn[ks];
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) vr[i] = vn[i];
   }
 
-  // ---- merge row slots within the wave (lanes with equal dc), then waves through LDS ----
+  // ---- merge row slots inside the wave, then the four waves through LDS ----
 #pragma unroll
-  for (int hh = 0; hh < 8; ++hh)
+  for (int hh = 0; hh < G; ++hh)
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       float a = acc[hh][e];
+#pragma unroll
       for (int o = DCH; o < kWave; o <<= 1) a += __shfl_xor(a, o);
       acc[hh][e] = a;
     }
@@ -185,7 +224,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
   l_run += __shfl_xor(l_run, 32);
   if (lane < DCH) {
 #pragma unroll
-    for (int hh = 0; hh < 8; ++hh)
+    for (int hh = 0; hh < G; ++hh)
 #pragma unroll
       for (int e = 0; e < 8; ++e) acc_lds[wave][hh][8 * dc + e] = acc[hh][e];
   }
@@ -194,86 +233,147 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
     l_lds[wave][col] = l_run;
   }
   __syncthreads();
-  const int nsplit = nsplit_max;
-  for (int idx = threadIdx.x; idx < G * (D + 2); idx += kDecThreads) {
-    const int hh = idx / (D + 2);
-    const int f = idx % (D + 2);
+
+  const int pair = b * Hkv + kvh;
+  float *orow = out + (static_cast<size_t>(b) * Hq + kvh * G) * D;
+  if (nsp == 1) {
+    for (int idx = threadIdx.x; idx < G * D; idx += kDecThreads) {
+      const int hh = idx / D, dd = idx % D;
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, m_lds[w][hh]);
+      float L = 0.f, A = 0.f;
+#pragma unroll
+      for (int w = 0; w < kDecWaves; ++w) {
+        const float sc = (m_lds[w][hh] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_lds[w][hh] - M);
+        L += sc * l_lds[w][hh];
+        A += sc * acc_lds[w][hh][dd];
+      }
+      orow[idx] = A / L;
+    }
+    return;
+  }
+  float *rec = ws.part + (static_cast<size_t>(pair) * nsplit_max + split) * REC;
+  for (int idx = threadIdx.x; idx < REC; idx += kDecThreads) {
+    const int hh = idx / (D + 2), f = idx % (D + 2);
     float M = -INFINITY;
 #pragma unroll
     for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, m_lds[w][hh]);
-    float val = 0.f;
-    if (f == 0) {
-      val = M;
-    } else {
+    float val = M;
+    if (f > 0) {
+      val = 0.f;
 #pragma unroll
       for (int w = 0; w < kDecWaves; ++w) {
         const float sc = (m_lds[w][hh] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_lds[w][hh] - M);
         val += sc * (f == 1 ? l_lds[w][hh] : acc_lds[w][hh][f - 2]);
       }
     }
-    const int h = kvh * G + hh;
-    ws[((static_cast<size_t>(b) * Hq + h) * nsplit + split) * (D + 2) + f] = val;
+    rec[idx] = val;
   }
 }
 
-template <int D>
+// Merge the split partials of one (kv-head, request); kv-head 0 advances the length.
+template <int D, int G>
 __global__ __launch_bounds__(kDecThreads) void decode_combine_kernel(int32_t *__restrict__ cache_len,
-                                                                     const float *__restrict__ ws,
-                                                                     float *__restrict__ out, int32_t *status, int Hq,
-                                                                     int rows_per_split, int nsplit_max) {
-  __shared__ int s_ok;
-  if (!block_status_clear(status, &s_ok)) return;
-  const int b = blockIdx.x;
-  const int len = cache_len[b];
-  const int nsp = (len + 1 + rows_per_split - 1) / rows_per_split;
-  for (int idx = threadIdx.x; idx < Hq * D; idx += kDecThreads) {
-    const int h = idx / D;
-    const int d = idx % D;
-    const float *part = ws + (static_cast<size_t>(b) * Hq + h) * nsplit_max * (D + 2);
+                                                                     float *__restrict__ out, DecodeWs ws, int Hkv,
+                                                                     int nsplit_max) {
+  constexpr int REC = G * (D + 2);
+  __shared__ float m_s[G];
+  __shared__ float l_s[G];
+  const int kvh = blockIdx.x;
+  const int b = blockIdx.y;
+  const int nsp = ws.nsplit[b];
+  if (nsp == 0) return;   // the request could not append this step
+  if (kvh == 0 && threadIdx.x == 0) cache_len[b] += 1;   // nothing else reads it in this kernel
+  if (nsp == 1) return;   // the split kernel wrote the output itself
+  const int pair = b * Hkv + kvh;
+  const float *recs = ws.part + static_cast<size_t>(pair) * nsplit_max * REC;
+  if (threadIdx.x < G) {
+    const int o = threadIdx.x * (D + 2);
     float M = -INFINITY;
-    for (int sp = 0; sp < nsp; ++sp) M = fmaxf(M, part[sp * (D + 2)]);
-    float L = 0.f, A = 0.f;
+    for (int sp = 0; sp < nsp; ++sp) M = fmaxf(M, recs[sp * REC + o]);
+    float L = 0.f;
     for (int sp = 0; sp < nsp; ++sp) {
-      const float ms = part[sp * (D + 2)];
-      const float sc = (ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - M);
-      L += sc * part[sp * (D + 2) + 1];
-      A += sc * part[sp * (D + 2) + 2 + d];
+      const float ms = recs[sp * REC + o];
+      L += (ms == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ms - M)) * recs[sp * REC + o + 1];
     }
-    out[(static_cast<size_t>(b) * Hq + h) * D + d] = A / L;
+    m_s[threadIdx.x] = M;
+    l_s[threadIdx.x] = L;
   }
   __syncthreads();
-  if (threadIdx.x == 0) cache_len[b] = len + 1;
-}
-
-template <int D>
-static void launch_decode_d(dim3 grid, int batch, int Hq, int Hkv, int max_ctx, int rows_per_split, int nsplit,
-                            uint16_t *kc, uint16_t *vc, const int64_t *row_off, const int32_t *row_cap,
-                            int32_t *cache_len, const uint8_t *row_role, const uint16_t *q, const uint16_t *k_new,
-                            const uint16_t *v_new, float scale_log2, float *out, float *ws, int32_t *status,
-                            hipStream_t stream) {
-  decode_split_kernel<D><<<grid, dim3(kDecThreads), 0, stream>>>(kc, vc, row_off, row_cap, cache_len, row_role, q,
-                                                                 k_new, v_new, ws, status, Hq, Hkv, rows_per_split,
-                                                                 nsplit, max_ctx, scale_log2);
-  decode_combine_kernel<D><<<dim3(batch), dim3(kDecThreads), 0, stream>>>(cache_len, ws, out, status, Hq,
-                                                                          rows_per_split, nsplit);
+  float *orow = out + (static_cast<size_t>(b) * Hkv * G + kvh * G) * D;
+  for (int idx = threadIdx.x; idx < G * D; idx += kDecThreads) {
+    const int hh = idx / D, dd = idx % D;
+    const float M = m_s[hh];
+    float A = 0.f;
+    for (int sp = 0; sp < nsp; ++sp) {
+      const float ms = recs[sp * REC + hh * (D + 2)];
+      const float sc = (ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - M);
+      A += sc * recs[sp * REC + hh * (D + 2) + 2 + dd];
+    }
+    orow[idx] = A / l_s[hh];
+  }
 }
 
 int decode_num_splits(int max_ctx, int rows_per_split) { return (max_ctx + rows_per_split - 1) / rows_per_split; }
 
+size_t decode_ws_layout(int batch, int Hkv, int G, int D, int nsplit, DecodeWs *ws, char *base) {
+  const size_t nbytes = (static_cast<size_t>(batch) * sizeof(int32_t) + 255) / 256 * 256;
+  const size_t pbytes = static_cast<size_t>(batch) * Hkv * nsplit * G * (D + 2) * sizeof(float);
+  if (ws) {
+    ws->nsplit = reinterpret_cast<int32_t *>(base);
+    ws->part = reinterpret_cast<float *>(base + nbytes);
+  }
+  return nbytes + pbytes;
+}
+
+template <int D, int G>
+static void launch_decode_dg(dim3 grid, int batch, int Hkv, int max_ctx, int rows_per_split, int nsplit,
+                             uint16_t *kc, uint16_t *vc, const int64_t *row_off, const int32_t *row_cap,
+                             int32_t *cache_len, const uint8_t *row_role, const uint16_t *q, const uint16_t *k_new,
+                             const uint16_t *v_new, float scale_log2, float *out, DecodeWs ws, int32_t *status,
+                             hipStream_t stream) {
+  decode_kernel<D, G><<<grid, dim3(kDecThreads), 0, stream>>>(kc, vc, row_off, row_cap, cache_len, row_role, q, k_new,
+                                                              v_new, out, ws, status, Hkv, rows_per_split, nsplit,
+                                                              max_ctx, scale_log2);
+  decode_combine_kernel<D, G><<<dim3(Hkv, batch), dim3(kDecThreads), 0, stream>>>(cache_len, out, ws, Hkv, nsplit);
+}
+
 hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int rows_per_split, uint16_t *kc,
                          uint16_t *vc, const int64_t *row_off, const int32_t *row_cap, int32_t *cache_len,
                          const uint8_t *row_role, const uint16_t *q, const uint16_t *k_new, const uint16_t *v_new,
-                         float scale_log2, float *out, float *ws, int32_t *status, hipStream_t stream) {
+                         float scale_log2, float *out, void *ws_base, int32_t *status, hipStream_t stream) {
+  const int G = Hq / Hkv;
   const int nsplit = decode_num_splits(max_ctx, rows_per_split);
+  DecodeWs ws;
+  decode_ws_layout(batch, Hkv, G, D, nsplit, &ws, static_cast<char *>(ws_base));
   dim3 grid(nsplit, Hkv, batch);
-  if (D == 64)
-    launch_decode_d<64>(grid, batch, Hq, Hkv, max_ctx, rows_per_split, nsplit, kc, vc, row_off, row_cap, cache_len,
-                        row_role, q, k_new, v_new, scale_log2, out, ws, status, stream);
-  else if (D == 128)
-    launch_decode_d<128>(grid, batch, Hq, Hkv, max_ctx, rows_per_split, nsplit, kc, vc, row_off, row_cap, cache_len,
-                         row_role, q, k_new, v_new, scale_log2, out, ws, status, stream);
-  else
+#define DEC(DD, GG)                                                                                               \
+  case GG:                                                                                                        \
+    launch_decode_dg<DD, GG>(grid, batch, Hkv, max_ctx, rows_per_split, nsplit, kc, vc, row_off, row_cap,        \
+                             cache_len, row_role, q, k_new, v_new, scale_log2, out, ws, status, stream);          \
+    break;
+#define DEC_ALL_G(DD)                     \
+  switch (G) {                            \
+    DEC(DD, 1)                            \
+    DEC(DD, 2)                            \
+    DEC(DD, 3)                            \
+    DEC(DD, 4)                            \
+    DEC(DD, 5)                            \
+    DEC(DD, 6)                            \
+    DEC(DD, 7)                            \
+    DEC(DD, 8)                            \
+    default: return hipErrorInvalidValue; \
+  }
+  if (D == 64) {
+    DEC_ALL_G(64)
+  } else if (D == 128) {
+    DEC_ALL_G(128)
+  } else {
     return hipErrorInvalidValue;
+  }
+#undef DEC_ALL_G
+#undef DEC
   return hipGetLastError();
 }
 

@@ -17,6 +17,13 @@
 // entries (the ragged end of the key list and the causal diagonal); all
 // earlier steps are fully visible and skip the predicate.
 //
+// LDS is double-buffered: while step c is computed, the K rows of step c+1
+// stream straight into the other buffer (global_load_lds_dwordx4, no
+// registers) and its V rows into registers, which are written transposed
+// (V^T rows are d) after the step's MFMAs; one barrier per step.  The running
+// max is updated lazily: O and the sum are rescaled only when the max grows by
+// more than 2^8, so most steps skip the rescale (p stays below 2^8).
+//
 // The grid is persistent: workgroup w serves the queue of XCD (w mod 8); item i
 // belongs to queue i mod 8, and items are ordered so that one queue sees one
 // kv-head (Hkv = 8) or a fixed subset of kv-heads, which keeps the K/V a queue
@@ -42,18 +49,29 @@ __device__ __forceinline__ int virtual_to_pos(const TileDesc &t, const int32_t *
   return t.p0 + (vk - t.r1_len);
 }
 
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) const void global_void_t;
+
+// s_waitcnt with vmcnt(0) and the other counters left at their maximum (gfx9 encoding).
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 template <int D, int G>
 __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__restrict__ cu,
-                                                            const uint16_t *__restrict__ q,
-                                                            const uint16_t *__restrict__ k,
-                                                            const uint16_t *__restrict__ v, float *__restrict__ out,
-                                                            PrefillWs ws, int Hkv, float scale_log2) {
+                                                               const uint16_t *__restrict__ q,
+                                                               const uint16_t *__restrict__ k,
+                                                               const uint16_t *__restrict__ v, float *__restrict__ out,
+                                                               PrefillWs ws, int Hkv, float scale_log2) {
   constexpr int NT = G * kWave;
-  constexpr int DC = D / 8;    // 16-byte chunks per K row
-  constexpr int DS = D / 16;   // d steps of the S product
-  constexpr int DB = D / 32;   // 32-wide d blocks of the output
-  __shared__ __align__(16) uint16_t k_lds[kKeyChunk * D];   // [64 keys][D], chunk-swizzled
-  __shared__ __align__(16) uint16_t vt_lds[D * kKeyChunk];  // [D][64 keys], chunk-swizzled
+  constexpr int DC = D / 8;              // 16-byte chunks per K row
+  constexpr int DS = D / 16;             // d steps of the S product
+  constexpr int DB = D / 32;             // 32-wide d blocks of the output
+  constexpr int KROWS = kWave / DC;      // K rows filled by one direct-to-LDS wave instruction
+  constexpr int KINST = kKeyChunk / KROWS;   // such instructions per 64-key step
+  constexpr int VTASKS = 16 * DC;        // V tasks: (4 keys) x (8 d) each
+  constexpr int VPT = (VTASKS + NT - 1) / NT;
+  constexpr float kLazy = 8.f;           // rescale only when the running max grows by > 2^8
+  __shared__ __align__(16) uint16_t k_lds[2][kKeyChunk * D];   // [buf][64 keys][D], MFMA row order, swizzled
+  __shared__ __align__(16) uint16_t vt_lds[2][D * kKeyChunk];  // [buf][D][64 keys], swizzled
   __shared__ int s_item;
 
   const int Hq = Hkv * G;
@@ -78,6 +96,69 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
     const int h = kvh * G + wave;
     const int nv = tile_key_count(t);
     const int nF = nv - t.ndiag;
+    const uint16_t *kh = k + static_cast<size_t>(kvh) * D;
+    const uint16_t *vh = v + static_cast<size_t>(kvh) * D;
+    const size_t tok_stride = static_cast<size_t>(Hkv) * D;
+
+    // K: direct-to-LDS, one 16-byte chunk per lane.  LDS row m holds key perm(m); the
+    // lane that fills (row m, slot c') fetches chunk c' ^ (m & 7), which is the swizzle.
+    // Keys past the list end repeat its first key; their scores are masked anyway.
+    auto stage_k = [&](int c, int buf) {
+      for (int i = wave; i < KINST; i += G) {
+        const int m = i * KROWS + lane / DC;
+        const int cslot = lane % DC;
+        const int r = (m & 32) | perm32(m & 31);
+        int vk = c * kKeyChunk + r;
+        if (vk >= nv) vk = 0;
+        const int p = virtual_to_pos(t, npos, vk);
+        const uint16_t *src = kh + static_cast<size_t>(base + p) * tok_stride + (cslot ^ (m & 7)) * 8;
+        // C-style casts: these change address spaces, which reinterpret_cast cannot do
+        __builtin_amdgcn_global_load_lds((global_void_t *)src, (lds_void_t *)&k_lds[buf][i * KROWS * D], 16, 0, 0);
+      }
+    };
+    // V: 4 keys x 8 d per task through registers, written transposed (V^T rows are d).
+    auto load_v = [&](int c, u32x4 (&vr)[VPT][4]) {
+#pragma unroll
+      for (int j = 0; j < VPT; ++j) {
+        const int task = threadIdx.x + j * NT;
+        const int dg = task % DC;
+        const int kq = task / DC;          // group of 4 keys, 0..15
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int vk = c * kKeyChunk + kq * 4 + i;
+          vr[j][i] = u32x4{0u, 0u, 0u, 0u};
+          if (task < VTASKS && vk < nv) {
+            const int p = virtual_to_pos(t, npos, vk);
+            vr[j][i] = *reinterpret_cast<const u32x4 *>(vh + static_cast<size_t>(base + p) * tok_stride + dg * 8);
+          }
+        }
+      }
+    };
+    auto store_v = [&](int buf, const u32x4 (&vr)[VPT][4]) {
+#pragma unroll
+      for (int j = 0; j < VPT; ++j) {
+        const int task = threadIdx.x + j * NT;
+        if (task >= VTASKS) continue;
+        const int dg = task % DC;
+        const int kq = task / DC;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {   // d = 8*dg + e: element e of the 4 keys
+          const uint32_t a0 = vr[j][0][e >> 1], a1 = vr[j][1][e >> 1];
+          const uint32_t a2 = vr[j][2][e >> 1], a3 = vr[j][3][e >> 1];
+          uint2 o;
+          if (e & 1) {
+            o.x = (a0 >> 16) | (a1 & 0xFFFF0000u);
+            o.y = (a2 >> 16) | (a3 & 0xFFFF0000u);
+          } else {
+            o.x = (a0 & 0xFFFFu) | (a1 << 16);
+            o.y = (a2 & 0xFFFFu) | (a3 << 16);
+          }
+          const int dr = dg * 8 + e;
+          const int chunk = (kq >> 1) ^ (dr & 7);
+          *reinterpret_cast<uint2 *>(&vt_lds[buf][(dr * 8 + chunk) * 8 + (kq & 1) * 4]) = o;
+        }
+      }
+    };
 
     // Q^T fragments (B operand): lane (row n, half g) holds d = 16*ds + 8*g .. +7.
     bf16x8 qf[DS];
@@ -95,52 +176,25 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
     f32x16 oacc[DB];
 #pragma unroll
     for (int i = 0; i < DB; ++i) oacc[i] = f32x16{};
-    float m_run = -INFINITY;
+    float m_run = -INFINITY;   // running max in the log2 domain (lags by at most kLazy)
     float l_run = 0.f;
 
     const int nchunks = (nv + kKeyChunk - 1) / kKeyChunk;
+    u32x4 vr[VPT][4];
+    stage_k(0, 0);
+    load_v(0, vr);
+    store_v(0, vr);
+    wait_vmem();
+    __syncthreads();
+
     for (int c = 0; c < nchunks; ++c) {
+      const int cur = c & 1;
+      const bool more = c + 1 < nchunks;
+      if (more) {   // next step's K straight into the other buffer, its V into registers
+        stage_k(c + 1, cur ^ 1);
+        load_v(c + 1, vr);
+      }
       const int vk0 = c * kKeyChunk;
-      // ---- stage K (row-major, MFMA row order) and V^T into LDS ----
-      for (int task = threadIdx.x; task < kKeyChunk * DC; task += NT) {
-        const int r = task / DC;
-        const int cc = task % DC;
-        const int vk = vk0 + r;
-        u32x4 w = {0u, 0u, 0u, 0u};
-        if (vk < nv) {
-          const int p = virtual_to_pos(t, npos, vk);
-          w = *reinterpret_cast<const u32x4 *>(k + (static_cast<size_t>(base + p) * Hkv + kvh) * D + cc * 8);
-        }
-        const int m = (r & 32) | perm32(r & 31);
-        *reinterpret_cast<u32x4 *>(k_lds + (m * DC + (cc ^ (m & 7))) * 8) = w;
-      }
-      for (int task = threadIdx.x; task < 8 * DC; task += NT) {
-        const int dg = task % DC;   // 8 consecutive d
-        const int kg = task / DC;   // 8 consecutive keys
-        u32x4 rows[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int vk = vk0 + kg * 8 + i;
-          rows[i] = u32x4{0u, 0u, 0u, 0u};
-          if (vk < nv) {
-            const int p = virtual_to_pos(t, npos, vk);
-            rows[i] = *reinterpret_cast<const u32x4 *>(v + (static_cast<size_t>(base + p) * Hkv + kvh) * D + dg * 8);
-          }
-        }
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {   // d = 8*dg + j: gather element j of the 8 keys
-          u32x4 o;
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const uint32_t a = rows[2 * u][j >> 1];
-            const uint32_t bb = rows[2 * u + 1][j >> 1];
-            o[u] = (j & 1) ? ((a >> 16) | (bb & 0xFFFF0000u)) : ((a & 0xFFFFu) | (bb << 16));
-          }
-          const int dr = dg * 8 + j;
-          *reinterpret_cast<u32x4 *>(vt_lds + (dr * 8 + (kg ^ (dr & 7))) * 8) = o;
-        }
-      }
-      __syncthreads();
 
       // ---- S^T = K . Q^T for two 32-key blocks ----
       f32x16 sacc[2];
@@ -150,32 +204,38 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
         const int m = kb * 32 + n;
 #pragma unroll
         for (int ds = 0; ds < DS; ++ds) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8 *>(k_lds + (m * DC + ((2 * ds + g) ^ (m & 7))) * 8);
+          const bf16x8 a =
+              *reinterpret_cast<const bf16x8 *>(&k_lds[cur][(m * DC + ((2 * ds + g) ^ (m & 7))) * 8]);
           sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ds], sacc[kb], 0, 0, 0);
         }
       }
 
       // ---- mask (ragged end / causal diagonal only), online softmax ----
-      const bool need_mask = vk0 + kKeyChunk > nF;
+      if (vk0 + kKeyChunk > nF) {
+        // Row n sees every key before the diagonal block and diagonal keys j <= n:
+        // virtual key vk is visible iff vk < min(nv, nF + n + 1).  One compare and a
+        // select per element, no divergent branches.
+        const int lim = min(nv, nF + n + 1) - vk0;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            sacc[kb][e] = (kb * 32 + acc_key(e, g) < lim) ? sacc[kb][e] : -INFINITY;
+      }
       float mloc = -INFINITY;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          float x = sacc[kb][e] * scale_log2;
-          if (need_mask) {
-            const int vk = vk0 + kb * 32 + acc_key(e, g);
-            const bool vis = vk < nF || (vk < nv && vk - nF <= n);
-            x = vis ? x : -INFINITY;
-          }
-          sacc[kb][e] = x;
-          mloc = fmaxf(mloc, x);
-        }
+        for (int e = 0; e < 16; ++e) mloc = fmaxf(mloc, sacc[kb][e]);
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32)) * scale_log2;
+      if (__any(mloc > m_run + kLazy)) {
+        const float m_new = fmaxf(m_run, mloc);
+        const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+        l_run *= corr;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) oacc[db] *= corr;
       }
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-      const float m_new = fmaxf(m_run, mloc);
-      const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
       float lsum = 0.f;
       bf16x8 pb[4];
 #pragma unroll
@@ -183,16 +243,14 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
         f32x8 lo, hi;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          lo[e] = __builtin_amdgcn_exp2f(sacc[kb][e] - m_new);
-          hi[e] = __builtin_amdgcn_exp2f(sacc[kb][8 + e] - m_new);
+          lo[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][e], scale_log2, -m_run));
+          hi[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][8 + e], scale_log2, -m_run));
           lsum += lo[e] + hi[e];
         }
         pb[2 * kb] = __builtin_convertvector(lo, bf16x8);
         pb[2 * kb + 1] = __builtin_convertvector(hi, bf16x8);
       }
-      l_run = l_run * corr + lsum;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) oacc[db] *= corr;
+      l_run += lsum;
 
       // ---- O^T += V^T . P^T ----
 #pragma unroll
@@ -200,10 +258,13 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
         const int dr = db * 32 + n;
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8 *>(vt_lds + (dr * 8 + ((2 * ks + g) ^ (dr & 7))) * 8);
+          const bf16x8 a =
+              *reinterpret_cast<const bf16x8 *>(&vt_lds[cur][(dr * 8 + ((2 * ks + g) ^ (dr & 7))) * 8]);
           oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[ks], oacc[db], 0, 0, 0);
         }
       }
+      if (more) store_v(cur ^ 1, vr);
+      wait_vmem();
       __syncthreads();
     }
 

@@ -105,7 +105,8 @@ class CompactCache:
     def decode(self, q, k_new, v_new, out, status, max_ctx: int, row_role: Optional[torch.Tensor] = None,
                stream=None) -> int:
         B, Hq, d = q.shape
-        key = (B, Hq, d, int(max_ctx))
+        Hkv = k_new.shape[1]
+        key = (B, Hq, Hkv, d, int(max_ctx))
         if self.ws_key != key:
             n = sonic.decode_workspace_bytes(B, Hq, d, int(max_ctx))
             self.ws = torch.empty(max(n, 256), dtype=torch.uint8, device=q.device)

@@ -145,20 +145,27 @@ def test_decode_workloads(idx, check):
 
 
 def test_decode_capacity_overflow():
+    """A request whose append would overflow is left unchanged; the others proceed."""
     H.need_gpu()
     lays = [W.RequestLayout(4, [10], [3], 2), W.RequestLayout(2, [5], [1], 1)]
     batch = W.make_batch("cap", lays, 4, 2, 64, seed=3, decode_steps=3)
     db, cache, ref = compacted(batch, np.array([1, 3]))
+    kc, vc, n, off = ref
     out = torch.full((2, 4, 64), 5.0, dtype=torch.float32, device="cuda")
     max_ctx = int(cache.row_cap_host.max())
     q, kn, vn = (bf16_to_device(x) for x in (batch.dec_q, batch.dec_k, batch.dec_v))
     assert cache.decode(q[0], kn[0], vn[0], out, db.status, max_ctx) == sonic.OK
     torch.cuda.synchronize()
     assert db.read_status() == 0
-    lens = cache.length.cpu().numpy().copy()
+    assert np.array_equal(cache.length.cpu().numpy(), n + 1)
     out.fill_(5.0)
     assert cache.decode(q[1], kn[1], vn[1], out, db.status, max_ctx) == sonic.OK   # request 0 is full now
     torch.cuda.synchronize()
     assert db.read_status() == sonic.ERR_CAPACITY
-    assert np.array_equal(cache.length.cpu().numpy(), lens)
-    assert torch.all(out == 5.0)
+    assert np.array_equal(cache.length.cpu().numpy(), n + np.array([1, 2]))
+    got = out.cpu().numpy()
+    assert np.all(got[0] == 5.0)
+    o, ln = int(off[1]), int(n[1])
+    want = OD.decode_step(batch.dec_q[1, 1], np.concatenate([kc[o:o + ln], batch.dec_k[:1, 1]]),
+                          np.concatenate([vc[o:o + ln], batch.dec_v[:1, 1]]), batch.dec_k[1, 1], batch.dec_v[1, 1])
+    H.assert_close(got[1], want, "request 1 after request 0 overflowed")
