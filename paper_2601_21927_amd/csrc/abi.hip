@@ -1,4 +1,5 @@
 // C ABI entry points: argument checks, workspace carving and kernel launches.
+#include <algorithm>
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
@@ -275,19 +276,13 @@ int32_t sonic_kv_compact(int32_t batch, int32_t total_tokens, int32_t max_seqlen
 }
 
 // ---------------------------------------------------------------- decode
-static int decode_rows_per_split(int32_t batch, int32_t Hkv, int32_t max_ctx) {
-  // about `target` workgroups over the whole batch (fewer, longer splits stream better), 64..4096 rows each
-  static const long target = [] {
-    const char *e = std::getenv("SONIC_DECODE_TARGET_BLOCKS");   // tuning override
-    const long v = e ? std::atol(e) : 0;
-    return v > 0 ? v : 512L;
-  }();
-  const long pairs = static_cast<long>(batch) * Hkv;
-  long rows = (static_cast<long>(max_ctx) * pairs + target - 1) / target;
-  rows = (rows + 63) / 64 * 64;
-  if (rows < 64) rows = 64;
-  if (rows > 4096) rows = 4096;
-  return static_cast<int>(rows);
+static int decode_rows_per_split(int32_t max_ctx) {
+  // rounds of 256 rows; more than one round per split only when that keeps the split
+  // count within what the merge stages in LDS (128)
+  constexpr long kRound = 256, kMaxSplits = 128;
+  long rounds = (static_cast<long>(max_ctx) + kRound * kMaxSplits - 1) / (kRound * kMaxSplits);
+  if (rounds < 1) rounds = 1;
+  return static_cast<int>(rounds * kRound);
 }
 
 static size_t decode_ws_bytes(int32_t batch, int32_t Hq, int32_t d, int32_t nsplit) {
@@ -298,7 +293,7 @@ static size_t decode_ws_bytes(int32_t batch, int32_t Hq, int32_t d, int32_t nspl
 size_t sonic_decode_workspace_bytes(int32_t batch, int32_t Hq, int32_t d, int32_t max_ctx) {
   if (batch <= 0 || Hq <= 0 || max_ctx <= 0) return 256;
   // enough for any kv-head count: the smallest split size bounds the split count
-  return align_up(decode_ws_bytes(batch, Hq, d, decode_num_splits(max_ctx, 64)), 256);
+  return align_up(decode_ws_bytes(batch, Hq, d, decode_num_splits(max_ctx, decode_rows_per_split(max_ctx))), 256);
 }
 
 int32_t sonic_compressed_decode(int32_t batch, int32_t Hq, int32_t Hkv, int32_t d, int32_t max_ctx, void *k_cache,
@@ -320,7 +315,7 @@ int32_t sonic_compressed_decode(int32_t batch, int32_t Hq, int32_t Hkv, int32_t 
   if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(q, 16) || !aligned(k_new, 16) ||
       !aligned(v_new, 16) || !aligned(out, 16) || !aligned(workspace, 256))
     return SONIC_ERR_INVALID_ARG;
-  const int rps = decode_rows_per_split(batch, Hkv, max_ctx);
+  const int rps = decode_rows_per_split(max_ctx);
   if (workspace_bytes < decode_ws_bytes(batch, Hq, d, decode_num_splits(max_ctx, rps))) return SONIC_ERR_WORKSPACE;
   hipError_t e = launch_decode(batch, Hq, Hkv, d, max_ctx, rps, static_cast<uint16_t *>(k_cache),
                                static_cast<uint16_t *>(v_cache), cache_row_off, cache_row_cap, cache_len, row_role,

@@ -3,8 +3,9 @@
 // decode_kernel: grid (split, kv-head, request), 4 waves.  A
 // split owns rows [split*R, split*R + R) of the request's context rows 0..len
 // (row len is the token being generated: it is read from k_new/v_new, and split 0
-// of each kv-head also appends it to the cache).  Each wave walks 16-row groups,
-// loading the next group's K and V while it works on the current one:
+// of each kv-head also appends it to the cache).  A split is processed in rounds
+// of 256 rows; each wave issues the loads of all four of its 16-row groups of a
+// round before working through them:
 //   scores    S^T (16 rows x 16 cols) = K . Q^T with v_mfma_f32_16x16x32_bf16;
 //             column c < G is q-head kvh*G + c, the other columns are zero;
 //   softmax   per q-head, online, fp32, exp2 with log2(e) folded into the scale;
@@ -27,6 +28,8 @@ namespace sonic {
 constexpr int kDecThreads = 256;
 constexpr int kDecWaves = kDecThreads / kWave;
 constexpr int kDecRowsPerGroup = 16;
+constexpr int kGroups = 4;                                           // groups per wave per round
+constexpr int kRoundRows = kGroups * kDecWaves * kDecRowsPerGroup;  // 256 rows per round
 
 struct DecodeWs {
   float *part;        // [B*Hkv][nsplit][G*(D+2)] partial (m[G], l[G], acc[G][D]) per split
@@ -66,7 +69,15 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_kernel(
   }
   const int nsp = (n_ctx + rows_per_split - 1) / rows_per_split;
   if (split == 0 && kvh == 0 && threadIdx.x == 0) ws.nsplit[b] = nsp;
-  if (split >= nsp) return;
+  if (split >= nsp) {
+    // an unused split leaves an empty record (max -inf, sum 0, acc 0) so that the merge can
+    // read every record without first waiting for the split count
+    if (nsp > 1) {
+      float *rec = ws.part + (static_cast<size_t>(b * Hkv + kvh) * nsplit_max + split) * REC;
+      for (int idx = threadIdx.x; idx < REC; idx += kDecThreads) rec[idx] = (idx % (D + 2) == 0) ? -INFINITY : 0.f;
+    }
+    return;
+  }
   const int r_begin = split * rows_per_split;
   const int r_end = min(n_ctx, r_begin + rows_per_split);
   const int64_t base = row_off[b];
@@ -131,83 +142,81 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_kernel(
   float m_run = -INFINITY;
   float l_run = 0.f;
 
-  constexpr int kStride = kDecWaves * kDecRowsPerGroup;
-  int r0 = r_begin + wave * kDecRowsPerGroup;
-  u32x4 kr[KS], vr[VPL];
-  if (r0 < r_end) {
-    load_k(r0, kr);
-    load_v(r0, vr);
-  }
-  for (; r0 < r_end; r0 += kStride) {
-    // prefetch the next group while this one is processed
-    u32x4 kn[KS], vn[VPL];
-    const int rn = r0 + kStride;
-    if (rn < r_end) {
-      load_k(rn, kn);
-      load_v(rn, vn);
-    }
-    f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+  // A round covers kRoundRows rows: wave w takes 16-row groups j*4 + w, j < kGroups.  All
+  // of a round's loads are issued before any of its groups is processed, so a wave keeps
+  // kGroups x (K + V) rows in flight instead of waiting one memory round trip per group.
+  for (int rb = r_begin; rb < r_end; rb += kRoundRows) {
+    u32x4 kr[kGroups][KS], vr[kGroups][VPL];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[ks]), qf[ks], sacc, 0, 0, 0);
-    // lane (col, quarter) holds rows r0 + 4*quarter + i, i = 0..3, of head col
-    float x[4];
-    float mloc = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = r0 + 4 * quarter + i;
-      bool vis = r < r_end;
-      if (vis && row_role != nullptr && r < len) vis = row_role[base + r] != kText;
-      x[i] = vis ? sacc[i] * scale_log2 : -INFINITY;
-      mloc = fmaxf(mloc, x[i]);
+    for (int j = 0; j < kGroups; ++j) {
+      const int r0 = rb + (j * kDecWaves + wave) * kDecRowsPerGroup;
+      load_k(r0, kr[j]);
+      load_v(r0, vr[j]);
     }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-    const float m_new = fmaxf(m_run, mloc);
-    const float corr = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-    float psum = 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float p = (m_new == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(x[i] - m_new);
-      psum += p;
-      if (col < 8) p_lds[wave][4 * quarter + i][col] = p;
-    }
-    m_run = m_new;
-    l_run = l_run * corr + psum;
-    if (quarter == 0 && col < 8) corr_lds[wave][col] = corr;
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    for (int j = 0; j < kGroups; ++j) {
+      const int r0 = rb + (j * kDecWaves + wave) * kDecRowsPerGroup;
+      if (r0 >= r_end) break;   // uniform across the wave
+      f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[j][ks]), qf[ks], sacc, 0, 0, 0);
+      // lane (col, quarter) holds rows r0 + 4*quarter + i, i = 0..3, of head col
+      float x[4];
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = r0 + 4 * quarter + i;
+        bool vis = r < r_end;
+        // (the clamped index keeps the role load inside the request's rows even when unused)
+        if (row_role != nullptr) vis = vis && (r >= len || row_role[base + max(0, min(r, len - 1))] != kText);
+        x[i] = vis ? sacc[i] * scale_log2 : -INFINITY;
+        mloc = fmaxf(mloc, x[i]);
+      }
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+      const float m_new = fmaxf(m_run, mloc);
+      const float corr = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+      float psum = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = (m_new == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(x[i] - m_new);
+        psum += p;
+        if (col < 8) p_lds[wave][4 * quarter + i][col] = p;
+      }
+      m_run = m_new;
+      l_run = l_run * corr + psum;
+      if (quarter == 0 && col < 8) corr_lds[wave][col] = corr;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
 #pragma unroll
-    for (int hh = 0; hh < G; ++hh) {
-      const float c = corr_lds[wave][hh];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[hh][e] *= c;
-    }
-#pragma unroll
-    for (int i = 0; i < VPL; ++i) {
-      const int rr = rq + i * ROWQ;
-      float vv[8];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        vv[2 * j] = bf16_lo(vr[i][j]);
-        vv[2 * j + 1] = bf16_hi(vr[i][j]);
-      }
-#pragma unroll
       for (int hh = 0; hh < G; ++hh) {
-        const float p = p_lds[wave][rr][hh];
+        const float c = corr_lds[wave][hh];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[hh][e] = fmaf(p, vv[e], acc[hh][e]);
+        for (int e = 0; e < 8; ++e) acc[hh][e] *= c;
       }
+#pragma unroll
+      for (int i = 0; i < VPL; ++i) {
+        const int rr = rq + i * ROWQ;
+        float vv[8];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          vv[2 * w] = bf16_lo(vr[j][i][w]);
+          vv[2 * w + 1] = bf16_hi(vr[j][i][w]);
+        }
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+          const float p = p_lds[wave][rr][hh];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[hh][e] = fmaf(p, vv[e], acc[hh][e]);
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kr[ks] = kn[ks];
-#pragma unroll
-    for (int i = 0; i < VPL; ++i) vr[i] = vn[i];
   }
 
   // ---- merge row slots inside the wave, then the four waves through LDS ----
@@ -273,45 +282,66 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_kernel(
 }
 
 // Merge the split partials of one (kv-head, request); kv-head 0 advances the length.
+// The split maxima and sums are staged in LDS first, so every global load of the
+// merge is independent of the others.
+constexpr int kMaxSplits = 128;
+
 template <int D, int G>
 __global__ __launch_bounds__(kDecThreads) void decode_combine_kernel(int32_t *__restrict__ cache_len,
                                                                      float *__restrict__ out, DecodeWs ws, int Hkv,
                                                                      int nsplit_max) {
   constexpr int REC = G * (D + 2);
-  __shared__ float m_s[G];
-  __shared__ float l_s[G];
+  __shared__ float m_s[kMaxSplits][G];
+  __shared__ float w_s[kMaxSplits][G];   // weight of each split: exp2(m_s - M) / L
+  __shared__ float M_s[G];
+  __shared__ float L_s[G];
   const int kvh = blockIdx.x;
   const int b = blockIdx.y;
-  const int nsp = ws.nsplit[b];
-  if (nsp == 0) return;   // the request could not append this step
-  if (kvh == 0 && threadIdx.x == 0) cache_len[b] += 1;   // nothing else reads it in this kernel
-  if (nsp == 1) return;   // the split kernel wrote the output itself
   const int pair = b * Hkv + kvh;
   const float *recs = ws.part + static_cast<size_t>(pair) * nsplit_max * REC;
+  // every record of the launch is valid (unused splits wrote empty ones), so the split
+  // count and the records are fetched together
+  const int nsp = ws.nsplit[b];
+  for (int t = threadIdx.x; t < nsplit_max * G; t += kDecThreads) {
+    const int sp = t / G, hh = t % G;
+    m_s[sp][hh] = recs[sp * REC + hh * (D + 2)];
+    w_s[sp][hh] = recs[sp * REC + hh * (D + 2) + 1];   // the split's sum, for now
+  }
+  if (nsp == 0) return;   // the request could not append this step (uniform per block)
+  if (kvh == 0 && threadIdx.x == 0) cache_len[b] += 1;   // nothing else reads it in this kernel
+  if (nsp == 1) return;   // the split kernel wrote the output itself
+  __syncthreads();
   if (threadIdx.x < G) {
-    const int o = threadIdx.x * (D + 2);
+    const int hh = threadIdx.x;
     float M = -INFINITY;
-    for (int sp = 0; sp < nsp; ++sp) M = fmaxf(M, recs[sp * REC + o]);
+    for (int sp = 0; sp < nsplit_max; ++sp) M = fmaxf(M, m_s[sp][hh]);
     float L = 0.f;
-    for (int sp = 0; sp < nsp; ++sp) {
-      const float ms = recs[sp * REC + o];
-      L += (ms == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ms - M)) * recs[sp * REC + o + 1];
-    }
-    m_s[threadIdx.x] = M;
-    l_s[threadIdx.x] = L;
+    for (int sp = 0; sp < nsplit_max; ++sp)
+      L += (m_s[sp][hh] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_s[sp][hh] - M)) * w_s[sp][hh];
+    M_s[hh] = M;
+    L_s[hh] = L;
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < nsplit_max * G; t += kDecThreads) {
+    const int sp = t / G, hh = t % G;
+    w_s[sp][hh] = (m_s[sp][hh] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_s[sp][hh] - M_s[hh]) / L_s[hh];
   }
   __syncthreads();
   float *orow = out + (static_cast<size_t>(b) * Hkv * G + kvh * G) * D;
   for (int idx = threadIdx.x; idx < G * D; idx += kDecThreads) {
     const int hh = idx / D, dd = idx % D;
-    const float M = m_s[hh];
+    const float *col = recs + hh * (D + 2) + 2 + dd;
     float A = 0.f;
-    for (int sp = 0; sp < nsp; ++sp) {
-      const float ms = recs[sp * REC + hh * (D + 2)];
-      const float sc = (ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - M);
-      A += sc * recs[sp * REC + hh * (D + 2) + 2 + dd];
+    int sp = 0;
+    for (; sp + 8 <= nsplit_max; sp += 8) {   // eight independent loads in flight
+      float a[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) a[u] = col[(sp + u) * REC];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) A += w_s[sp + u][hh] * a[u];
     }
-    orow[idx] = A / l_s[hh];
+    for (; sp < nsplit_max; ++sp) A += w_s[sp][hh] * col[sp * REC];
+    orow[idx] = A;
   }
 }
 

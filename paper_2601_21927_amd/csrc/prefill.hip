@@ -17,10 +17,11 @@
 // entries (the ragged end of the key list and the causal diagonal); all
 // earlier steps are fully visible and skip the predicate.
 //
-// LDS is double-buffered: while step c is computed, the K rows of step c+1
-// stream straight into the other buffer (global_load_lds_dwordx4, no
-// registers) and its V rows into registers, which are written transposed
-// (V^T rows are d) after the step's MFMAs; one barrier per step.  The running
+// LDS is double-buffered: while step c is computed, the K and V rows of step
+// c+1 stream straight into the other buffer (global_load_lds_dwordx4, no
+// registers); one barrier per step.  V stays row-major in LDS and the V^T
+// operand of the second product is read with ds_read_b64_tr_b16, which
+// transposes 16-bit elements across each group of 16 lanes.  The running
 // max is updated lazily: O and the sum are rescaled only when the max grows by
 // more than 2^8, so most steps skip the rescale (p stays below 2^8).
 //
@@ -51,9 +52,23 @@ __device__ __forceinline__ int virtual_to_pos(const TileDesc &t, const int32_t *
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) const void global_void_t;
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
 
 // s_waitcnt with vmcnt(0) and the other counters left at their maximum (gfx9 encoding).
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// LDS bank swizzles (XOR on the 16-byte chunk index of a row), chosen so that the
+// reads below are conflict-free whether a pass covers 16 lanes of 32 banks or
+// 32 lanes of 64 banks.
+//   K rows are read with ds_read_b128, 16 rows at one chunk per pass;
+//   V rows are read with ds_read_b64_tr_b16, 4 rows x 4 chunks per pass.
+template <int D> __device__ __forceinline__ int swz_k(int m) {
+  return D == 128 ? (m & 15) : ((m & 7) ^ ((m >> 3) & 1));
+}
+template <int D> __device__ __forceinline__ int swz_v(int r) {
+  return D == 128 ? ((4 * (r & 3)) ^ (2 * ((r >> 1) & 1))) : (2 * (r & 3));
+}
 
 template <int D, int G>
 __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__restrict__ cu,
@@ -61,17 +76,14 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
                                                                const uint16_t *__restrict__ k,
                                                                const uint16_t *__restrict__ v, float *__restrict__ out,
                                                                PrefillWs ws, int Hkv, float scale_log2) {
-  constexpr int NT = G * kWave;
-  constexpr int DC = D / 8;              // 16-byte chunks per K row
+  constexpr int DC = D / 8;              // 16-byte chunks per K/V row
   constexpr int DS = D / 16;             // d steps of the S product
   constexpr int DB = D / 32;             // 32-wide d blocks of the output
-  constexpr int KROWS = kWave / DC;      // K rows filled by one direct-to-LDS wave instruction
-  constexpr int KINST = kKeyChunk / KROWS;   // such instructions per 64-key step
-  constexpr int VTASKS = 16 * DC;        // V tasks: (4 keys) x (8 d) each
-  constexpr int VPT = (VTASKS + NT - 1) / NT;
+  constexpr int ROWS_PER_INST = kWave / DC;        // rows filled by one direct-to-LDS wave instruction
+  constexpr int INSTS = kKeyChunk / ROWS_PER_INST;  // such instructions per tensor per 64-key step
   constexpr float kLazy = 8.f;           // rescale only when the running max grows by > 2^8
-  __shared__ __align__(16) uint16_t k_lds[2][kKeyChunk * D];   // [buf][64 keys][D], MFMA row order, swizzled
-  __shared__ __align__(16) uint16_t vt_lds[2][D * kKeyChunk];  // [buf][D][64 keys], swizzled
+  __shared__ __align__(16) uint16_t k_lds[2][kKeyChunk * D];   // [buf][64 keys][D], MFMA row order
+  __shared__ __align__(16) uint16_t v_lds[2][kKeyChunk * D];   // [buf][64 keys][D], key order
   __shared__ int s_item;
 
   const int Hq = Hkv * G;
@@ -81,6 +93,13 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
   const int g = lane >> 5;
   const int xcd = blockIdx.x % kNumXcd;
   const int nitems = ws.ctrl[0] * Hkv;
+
+  // Transposed-read geometry of the P.V operand (fixed per lane): 16-lane group q,
+  // index i.  Lane i of a group receives d = base + i for keys kbase + 4h + e.
+  const int tq = lane >> 4;
+  const int ti = lane & 15;
+  const int v_row_off = 8 * (tq >> 1) + (ti >> 2);      // + 16*ks + 4*h
+  const int v_d_off = 16 * (tq & 1) + 4 * (ti & 3);     // + 32*db
 
   for (;;) {
     if (threadIdx.x == 0) s_item = atomicAdd(&ws.ctrl[8 + xcd], 1) * kNumXcd + xcd;
@@ -100,67 +119,29 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
     const uint16_t *vh = v + static_cast<size_t>(kvh) * D;
     const size_t tok_stride = static_cast<size_t>(Hkv) * D;
 
-    // K: direct-to-LDS, one 16-byte chunk per lane.  LDS row m holds key perm(m); the
-    // lane that fills (row m, slot c') fetches chunk c' ^ (m & 7), which is the swizzle.
-    // Keys past the list end repeat its first key; their scores are masked anyway.
-    auto stage_k = [&](int c, int buf) {
-      for (int i = wave; i < KINST; i += G) {
-        const int m = i * KROWS + lane / DC;
+    // Both tensors go straight to LDS, one 16-byte chunk per lane: the lane that fills
+    // (row m, slot s) fetches chunk s ^ swizzle(m).  K row m holds key perm32(m) (MFMA
+    // row order); V row r holds key r.  Keys past the list end repeat its first key:
+    // their scores are masked, so they contribute exactly zero.
+    auto stage = [&](int c, int buf) {
+      for (int i = wave; i < 2 * INSTS; i += G) {
+        const bool is_v = i >= INSTS;
+        const int ii = is_v ? i - INSTS : i;
+        const int m = ii * ROWS_PER_INST + lane / DC;
         const int cslot = lane % DC;
-        const int r = (m & 32) | perm32(m & 31);
+        const int r = is_v ? m : ((m & 32) | perm32(m & 31));
         int vk = c * kKeyChunk + r;
         if (vk >= nv) vk = 0;
         const int p = virtual_to_pos(t, npos, vk);
-        const uint16_t *src = kh + static_cast<size_t>(base + p) * tok_stride + (cslot ^ (m & 7)) * 8;
+        const int src_chunk = cslot ^ (is_v ? swz_v<D>(m) : swz_k<D>(m));
+        const uint16_t *src = (is_v ? vh : kh) + static_cast<size_t>(base + p) * tok_stride + src_chunk * 8;
+        uint16_t *dst = is_v ? &v_lds[buf][ii * ROWS_PER_INST * D] : &k_lds[buf][ii * ROWS_PER_INST * D];
         // C-style casts: these change address spaces, which reinterpret_cast cannot do
-        __builtin_amdgcn_global_load_lds((global_void_t *)src, (lds_void_t *)&k_lds[buf][i * KROWS * D], 16, 0, 0);
-      }
-    };
-    // V: 4 keys x 8 d per task through registers, written transposed (V^T rows are d).
-    auto load_v = [&](int c, u32x4 (&vr)[VPT][4]) {
-#pragma unroll
-      for (int j = 0; j < VPT; ++j) {
-        const int task = threadIdx.x + j * NT;
-        const int dg = task % DC;
-        const int kq = task / DC;          // group of 4 keys, 0..15
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int vk = c * kKeyChunk + kq * 4 + i;
-          vr[j][i] = u32x4{0u, 0u, 0u, 0u};
-          if (task < VTASKS && vk < nv) {
-            const int p = virtual_to_pos(t, npos, vk);
-            vr[j][i] = *reinterpret_cast<const u32x4 *>(vh + static_cast<size_t>(base + p) * tok_stride + dg * 8);
-          }
-        }
-      }
-    };
-    auto store_v = [&](int buf, const u32x4 (&vr)[VPT][4]) {
-#pragma unroll
-      for (int j = 0; j < VPT; ++j) {
-        const int task = threadIdx.x + j * NT;
-        if (task >= VTASKS) continue;
-        const int dg = task % DC;
-        const int kq = task / DC;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {   // d = 8*dg + e: element e of the 4 keys
-          const uint32_t a0 = vr[j][0][e >> 1], a1 = vr[j][1][e >> 1];
-          const uint32_t a2 = vr[j][2][e >> 1], a3 = vr[j][3][e >> 1];
-          uint2 o;
-          if (e & 1) {
-            o.x = (a0 >> 16) | (a1 & 0xFFFF0000u);
-            o.y = (a2 >> 16) | (a3 & 0xFFFF0000u);
-          } else {
-            o.x = (a0 & 0xFFFFu) | (a1 << 16);
-            o.y = (a2 & 0xFFFFu) | (a3 << 16);
-          }
-          const int dr = dg * 8 + e;
-          const int chunk = (kq >> 1) ^ (dr & 7);
-          *reinterpret_cast<uint2 *>(&vt_lds[buf][(dr * 8 + chunk) * 8 + (kq & 1) * 4]) = o;
-        }
+        __builtin_amdgcn_global_load_lds((global_void_t *)src, (lds_void_t *)dst, 16, 0, 0);
       }
     };
 
-    // Q^T fragments (B operand): lane (row n, half g) holds d = 16*ds + 8*g .. +7.
+    // Q^T fragments (B operand of S): lane (row n, half g) holds d = 16*ds + 8*g .. +7.
     bf16x8 qf[DS];
     {
       const bool ok = n < t.nrows;
@@ -180,20 +161,13 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
     float l_run = 0.f;
 
     const int nchunks = (nv + kKeyChunk - 1) / kKeyChunk;
-    u32x4 vr[VPT][4];
-    stage_k(0, 0);
-    load_v(0, vr);
-    store_v(0, vr);
+    stage(0, 0);
     wait_vmem();
     __syncthreads();
 
     for (int c = 0; c < nchunks; ++c) {
       const int cur = c & 1;
-      const bool more = c + 1 < nchunks;
-      if (more) {   // next step's K straight into the other buffer, its V into registers
-        stage_k(c + 1, cur ^ 1);
-        load_v(c + 1, vr);
-      }
+      if (c + 1 < nchunks) stage(c + 1, cur ^ 1);   // next step streams into the other buffer
       const int vk0 = c * kKeyChunk;
 
       // ---- S^T = K . Q^T for two 32-key blocks ----
@@ -205,7 +179,7 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
 #pragma unroll
         for (int ds = 0; ds < DS; ++ds) {
           const bf16x8 a =
-              *reinterpret_cast<const bf16x8 *>(&k_lds[cur][(m * DC + ((2 * ds + g) ^ (m & 7))) * 8]);
+              *reinterpret_cast<const bf16x8 *>(&k_lds[cur][(m * DC + ((2 * ds + g) ^ swz_k<D>(m))) * 8]);
           sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ds], sacc[kb], 0, 0, 0);
         }
       }
@@ -252,18 +226,26 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
       }
       l_run += lsum;
 
-      // ---- O^T += V^T . P^T ----
+      // ---- O^T += V^T . P^T, V^T operands read transposed from row-major V ----
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const int dr = db * 32 + n;
+        const int dd = db * 32 + v_d_off;     // this lane's 4 d-values, a 4-aligned start
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
-          const bf16x8 a =
-              *reinterpret_cast<const bf16x8 *>(&vt_lds[cur][(dr * 8 + ((2 * ks + g) ^ (dr & 7))) * 8]);
-          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[ks], oacc[db], 0, 0, 0);
+          v4i16 part[2];
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const int r = 16 * ks + 4 * hh + v_row_off;
+            const int chunk = (dd >> 3) ^ swz_v<D>(r);
+            const uint16_t *pa = &v_lds[cur][r * D + chunk * 8 + (dd & 4)];
+            part[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)pa);
+          }
+          const u32x4 w = {__builtin_bit_cast(uint2, part[0]).x, __builtin_bit_cast(uint2, part[0]).y,
+                           __builtin_bit_cast(uint2, part[1]).x, __builtin_bit_cast(uint2, part[1]).y};
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w), pb[ks], oacc[db], 0,
+                                                             0, 0);
         }
       }
-      if (more) store_v(cur ^ 1, vr);
       wait_vmem();
       __syncthreads();
     }
