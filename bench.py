@@ -224,17 +224,17 @@ def main():
     if dominant == "prefill":
         roof = {"bound": "mfma", "achieved": round(prefill_tflops, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(prefill_tflops / PEAK_BF16_TFLOPS, 4),
-                "traffic": measured_traffic("prefill_kernel"), "kernel": "prefill (plan + prefill_kernel)"}
+                "traffic": measured_traffic("prefill"), "kernel": "sonic_segment_attn_prefill (plan + prefill_kernel)"}
     elif dominant == "decode":
         per_launch = decode_bytes / steps_dec
         ach = per_launch / (dc_ms * 1e-3 / steps_dec) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": measured_traffic("decode_split_kernel"),
-                "kernel": "decode step (decode_split_kernel + decode_combine_kernel)"}
+                "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": measured_traffic("decode"),
+                "kernel": "sonic_compressed_decode, one call (decode_kernel + decode_combine_kernel)"}
     else:
         roof = {"bound": "hbm", "achieved": round(compact_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(compact_gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic("compact_kernel"),
-                "kernel": "compact_kernel"}
+                "frac": round(compact_gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic("compact"),
+                "kernel": "sonic_kv_compact (compact_kernel)"}
 
     rec = {
         "metric": METRIC, "value": round(value, 1), "unit": "tok/s", "n_gpus": 1, "steps": args.steps,
