@@ -104,8 +104,14 @@ int32_t sonic_layout_stats_host(int32_t batch, const int32_t *cu_seqlens, const 
 /* Step 1: masked prefill attention                                          */
 /* ------------------------------------------------------------------------ */
 
-/* Bytes of device workspace sonic_segment_attn_prefill needs for this batch. */
-size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens);
+/*
+ * Bytes of device workspace sonic_segment_attn_prefill needs for this batch
+ * (0 for negative sizes or non-positive heads / head_dim).  It holds the
+ * per-block plan and a copy of each request's system and Nexus K/V rows, so
+ * it grows as total_tokens * num_kv_heads * head_dim * 4 bytes.
+ */
+size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens, int32_t num_kv_heads,
+                                     int32_t head_dim);
 
 /*
  * out[p][h] = sum_q softmax_q(scale * <q[p][h], k[q][g(h)]> + M[p][q]) * v[q][g(h)]
@@ -124,7 +130,7 @@ size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens);
  *   q                     device bf16 [T][Hq][d];  k, v: device bf16 [T][Hkv][d]
  *   softmax_scale         finite and > 0, e.g. 1/sqrt(d)
  *   out                   device fp32 [T][Hq][d] (fully written on success)
- *   workspace             device, >= sonic_prefill_workspace_bytes(B, T) bytes,
+ *   workspace             device, >= sonic_prefill_workspace_bytes(B, T, Hkv, d) bytes,
  *                         256-byte aligned; contents need no initialisation
  *   dev_status            device int32 (see conventions); SONIC_ERR_BAD_LAYOUT
  *                         is reported here and then no output is written

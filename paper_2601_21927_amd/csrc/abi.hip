@@ -9,8 +9,9 @@
 #include "common.h"
 
 namespace sonic {
-hipError_t launch_plan(int batch, int total_tokens, const int32_t *cu, const uint8_t *role, const int32_t *turn,
-                       PrefillWs ws, int32_t *status, hipStream_t stream);
+hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus, const int32_t *cu,
+                       const uint8_t *role, const int32_t *turn, const uint16_t *k, const uint16_t *v, PrefillWs ws,
+                       int32_t *status, hipStream_t stream);
 hipError_t prefill_occupancy(int D, int G, int *blocks);
 hipError_t launch_prefill(int D, int G, int grid, const int32_t *cu, const uint16_t *q, const uint16_t *k,
                           const uint16_t *v, float *out, PrefillWs ws, int Hkv, float scale_log2, hipStream_t stream);
@@ -27,7 +28,7 @@ hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int row
 
 namespace {
 
-constexpr int kAbiVersion = 1;
+constexpr int kAbiVersion = 2;
 constexpr double kLog2e = 1.4426950408889634;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -191,33 +192,42 @@ int32_t sonic_layout_stats_host(int32_t batch, const int32_t *cu, const uint8_t 
 }
 
 // ---------------------------------------------------------------- prefill
-static size_t prefill_ws_layout(int32_t batch, int32_t T, PrefillWs *ws, char *base) {
+static size_t prefill_ws_layout(int32_t batch, int32_t T, int32_t Hkv, int32_t d, PrefillWs *ws, char *base) {
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
     off = align_up(off + bytes, 256);
     return base ? base + o : nullptr;
   };
-  char *req = take(sizeof(ReqInfo) * static_cast<size_t>(batch > 0 ? batch : 1));
-  char *npos = take(sizeof(int32_t) * static_cast<size_t>(T > 0 ? T : 1));
-  char *runs = take(sizeof(int2) * static_cast<size_t>(T > 0 ? T : 1));
-  char *tiles = take(sizeof(TileDesc) * static_cast<size_t>(T > 0 ? T : 1));
-  char *order = take(sizeof(int32_t) * static_cast<size_t>(T > 0 ? T : 1));
+  const size_t B1 = static_cast<size_t>(batch > 0 ? batch : 1);
+  const size_t T1 = static_cast<size_t>(T > 0 ? T : 1);
+  char *req = take(sizeof(ReqInfo) * B1);
+  char *req_off = take(sizeof(int32_t) * B1);
+  char *ppos = take(sizeof(int32_t) * T1);
+  char *runs = take(sizeof(int2) * T1);
+  char *tiles = take(sizeof(TileDesc) * T1);
+  char *order = take(sizeof(int32_t) * T1);
   char *ctrl = take(sizeof(int32_t) * 16);
+  const size_t rows_bytes = T1 * static_cast<size_t>(Hkv > 0 ? Hkv : 1) * static_cast<size_t>(d > 0 ? d : 1) * 2;
+  char *kpre = take(rows_bytes);
+  char *vpre = take(rows_bytes);
   if (ws) {
     ws->req = reinterpret_cast<ReqInfo *>(req);
-    ws->nexus_pos = reinterpret_cast<int32_t *>(npos);
+    ws->req_off = reinterpret_cast<int32_t *>(req_off);
+    ws->prefix_pos = reinterpret_cast<int32_t *>(ppos);
     ws->runs = reinterpret_cast<int2 *>(runs);
     ws->tiles = reinterpret_cast<TileDesc *>(tiles);
     ws->order = reinterpret_cast<int32_t *>(order);
     ws->ctrl = reinterpret_cast<int32_t *>(ctrl);
+    ws->k_pre = reinterpret_cast<uint16_t *>(kpre);
+    ws->v_pre = reinterpret_cast<uint16_t *>(vpre);
   }
   return off;
 }
 
-size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens) {
-  if (batch < 0 || total_tokens < 0) return 0;
-  return prefill_ws_layout(batch, total_tokens, nullptr, nullptr);
+size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens, int32_t num_kv_heads, int32_t head_dim) {
+  if (batch < 0 || total_tokens < 0 || num_kv_heads <= 0 || head_dim <= 0) return 0;
+  return prefill_ws_layout(batch, total_tokens, num_kv_heads, head_dim, nullptr, nullptr);
 }
 
 int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t Hq, int32_t Hkv, int32_t d,
@@ -237,12 +247,13 @@ int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t 
     return SONIC_ERR_INVALID_ARG;
   if (static_cast<size_t>(total_tokens) * Hq * d >= (size_t(1) << 40)) return SONIC_ERR_UNSUPPORTED;
   PrefillWs ws;
-  const size_t need = prefill_ws_layout(batch, total_tokens, &ws, static_cast<char *>(workspace));
+  const size_t need = prefill_ws_layout(batch, total_tokens, Hkv, d, &ws, static_cast<char *>(workspace));
   if (workspace_bytes < need) return SONIC_ERR_WORKSPACE;
   DeviceInfo *di = nullptr;
   hipError_t e = device_info(&di);
   if (e != hipSuccess) return SONIC_ERR_HIP;
-  e = launch_plan(batch, total_tokens, cu_seqlens, role, turn_id, ws, dev_status, stream);
+  e = launch_plan(batch, total_tokens, Hkv, d, di->num_cus, cu_seqlens, role, turn_id,
+                  static_cast<const uint16_t *>(k), static_cast<const uint16_t *>(v), ws, dev_status, stream);
   if (e != hipSuccess) return SONIC_ERR_HIP;
   int grid = di->num_cus * di->prefill_blocks[d == 128][G];
   grid = (grid + kNumXcd - 1) / kNumXcd * kNumXcd;

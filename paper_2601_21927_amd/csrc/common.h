@@ -39,30 +39,30 @@ __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w 
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
 // Prefill work descriptor of one block of up to 32 query rows that share one
-// visible-key list.  The keys are taken, in this order, from
-//   [0, r0_end)                      contiguous, every row sees them
-//   nexus_pos[0, nx)                 gathered Nexus positions, every row sees them
-//   [r1_start, r1_start + r1_len)    contiguous, every row sees them
-//   [p0, p0 + ndiag)                 the block's own rows, causal (key j seen by row >= j)
-// All positions are request-local.
+// visible-key list.  Every list is two contiguous pieces:
+//   prefix rows [0, npre)            of the request's prefix copy (system prompt,
+//                                    then its Nexus tokens in order); every row sees them
+//   positions [seg_start, seg_start + seg_len)
+//                                    of the request itself; every row sees the first
+//                                    seg_len - ndiag, and the last ndiag are the block's
+//                                    own rows, causal (key j seen by row >= j)
+// Positions are request-local.
 struct TileDesc {
   int32_t req;
   int32_t p0;
   int32_t nrows;
-  int32_t r0_end;
-  int32_t nx;
-  int32_t r1_start;
-  int32_t r1_len;
+  int32_t npre;
+  int32_t seg_start;
+  int32_t seg_len;
   int32_t ndiag;
+  int32_t pad;
 };
 static_assert(sizeof(TileDesc) == 32, "descriptor is eight words");
 
 constexpr int kTileRows = 32;       // query rows per descriptor (one MFMA N block)
 constexpr int kKeyChunk = 64;       // keys per inner-loop step
 
-__host__ __device__ __forceinline__ int tile_key_count(const TileDesc &t) {
-  return t.r0_end + t.nx + t.r1_len + t.ndiag;
-}
+__host__ __device__ __forceinline__ int tile_key_count(const TileDesc &t) { return t.npre + t.seg_len; }
 __host__ __device__ __forceinline__ int tile_cost(const TileDesc &t) {
   return (tile_key_count(t) + kKeyChunk - 1) / kKeyChunk;
 }
@@ -73,15 +73,21 @@ struct ReqInfo {
   int32_t system;
   int32_t nexus_total;
   int32_t nruns;
+  int64_t cost;        // sum of tile_cost over the request's descriptors
+  int64_t pad;
 };
 
 // Device workspace of the prefill, carved from one caller buffer.
 struct PrefillWs {
   ReqInfo *req;        // [B]
-  int32_t *nexus_pos;  // [T]  request b's Nexus positions at offset cu[b]
+  int32_t *req_off;    // [B]  first slot of request b in `order`
+  int32_t *prefix_pos; // [T]  request b's prefix rows (system, then Nexus) at offset cu[b]: positions
   int2 *runs;          // [T]  (run start, Nexus count before it) at offset cu[b]
   TileDesc *tiles;     // [T]  request b's descriptors at offset cu[b]
-  int32_t *order;      // [T]  descriptor slots, most expensive first
+  int32_t *order;      // [T]  descriptor slots: requests by decreasing cost, inside a request by
+                       //      decreasing tile cost
+  uint16_t *k_pre;     // [T, Hkv, D] prefix copies of K and V, request b's rows at offset cu[b]
+  uint16_t *v_pre;
   int32_t *ctrl;       // [16] ctrl[0] = number of descriptors, ctrl[8 + x] = queue head of XCD x
 };
 

@@ -11,9 +11,16 @@
 //   * a current-query row sees the system prompt, every Nexus token and the
 //     current query up to itself; all bodies are removed (Eq.(4)).
 // Every block of at most 32 rows of one run therefore sees the same key list
-// apart from its own causal diagonal, and that list is "one contiguous range,
-// a prefix of the request's Nexus positions, one more contiguous range".  One
-// TileDesc per block encodes it; masked key blocks are never enumerated.
+// apart from its own causal diagonal.  With the request's system and Nexus rows
+// copied, in order, into one contiguous "prefix" (system prompt first, then the
+// Nexus tokens segment by segment), that list is "a leading part of the prefix,
+// then one contiguous range of the request ending in the block's own rows".
+// One TileDesc per block encodes it; masked key blocks are never enumerated.
+//
+// Work order: requests by decreasing total cost, and inside a request its blocks
+// by decreasing cost.  Blocks of one request run close together in time, so the
+// K/V rows they share (system prompt, Nexus tokens, bodies) stay in the L2 of
+// the XCD that serves them.
 #include "common.h"
 #include "scan.h"
 
@@ -55,13 +62,14 @@ __global__ __launch_bounds__(kPlanThreads) void plan_runs_kernel(const int32_t *
                                                                  int total_tokens, int32_t *status) {
   __shared__ int lds[kPlanThreads / kWave + 1];
   __shared__ int s_bad;
+  __shared__ unsigned long long s_cost;
   const int b = blockIdx.x;
   const int s = cu[b];
   const int e = cu[b + 1];
   if (s < 0 || e < s || e > total_tokens) {   // cu_seqlens itself is malformed
     if (threadIdx.x == 0) {
       raise_status(status, SONIC_ERR_BAD_LAYOUT);
-      ws.req[b] = ReqInfo{0, 0, 0, 0};
+      ws.req[b] = ReqInfo{0, 0, 0, 0, 0, 0};
     }
     return;
   }
@@ -69,8 +77,11 @@ __global__ __launch_bounds__(kPlanThreads) void plan_runs_kernel(const int32_t *
   if (threadIdx.x == 0) s_bad = 0;
   __syncthreads();
 
-  // Pass 1: grammar, Nexus positions, run starts (with the Nexus count before each).
-  int nexus_carry = 0, run_carry = 0;
+  // Pass 1: grammar, prefix rows (system and Nexus positions, in order), run starts
+  // with the number of prefix rows before each.  In a well-formed request the
+  // system rows come first, so the prefix is the system prompt followed by the
+  // Nexus tokens.
+  int pre_carry = 0, run_carry = 0, nexus_count = 0;
   for (int base = 0; base < L; base += kPlanThreads) {
     const int i = base + threadIdx.x;
     const bool in = i < L;
@@ -84,28 +95,32 @@ __global__ __launch_bounds__(kPlanThreads) void plan_runs_kernel(const int32_t *
       }
     }
     if (in && !legal_step(rp, tp, r, t)) s_bad = 1;
-    const bool is_nexus = in && r == kNexus;
+    const bool is_pre = in && (r == kSystem || r == kNexus);
     const bool run_start = in && (i == 0 || r != rp || (r == kText && t != tp));
-    int ntot, rtot;
-    const int nrank = block_flag_scan<kPlanThreads>(is_nexus, &ntot, lds);
+    int ptot, rtot, ntot;
+    const int prank = block_flag_scan<kPlanThreads>(is_pre, &ptot, lds);
     const int rrank = block_flag_scan<kPlanThreads>(run_start, &rtot, lds);
-    if (is_nexus) ws.nexus_pos[s + nexus_carry + nrank] = i;
-    if (run_start) ws.runs[s + run_carry + rrank] = make_int2(i, nexus_carry + nrank);
-    nexus_carry += ntot;
+    block_flag_scan<kPlanThreads>(in && r == kNexus, &ntot, lds);
+    if (is_pre) ws.prefix_pos[s + pre_carry + prank] = i;
+    if (run_start) ws.runs[s + run_carry + rrank] = make_int2(i, pre_carry + prank);
+    pre_carry += ptot;
     run_carry += rtot;
+    nexus_count += ntot;
   }
   __syncthreads();
   if (s_bad) {
     if (threadIdx.x == 0) {
       raise_status(status, SONIC_ERR_BAD_LAYOUT);
-      ws.req[b] = ReqInfo{0, 0, 0, 0};
+      ws.req[b] = ReqInfo{0, 0, 0, 0, 0, 0};
     }
     return;
   }
   const int nruns = run_carry;
-  const int k_tot = nexus_carry;
+  const int k_tot = nexus_count;
   int S = 0;
   if (L > 0 && role[s] == kSystem) S = nruns > 1 ? ws.runs[s + 1].x : L;
+  const int npre_all = S + k_tot;
+  if (threadIdx.x == 0) s_cost = 0ull;
 
   // Pass 2: descriptors, run by run.
   int tile_carry = 0;
@@ -122,94 +137,162 @@ __global__ __launch_bounds__(kPlanThreads) void plan_runs_kernel(const int32_t *
     const int toff = block_int_scan<kPlanThreads>(nt, &ttot, lds);
     if (in) {
       const int kind = role[s + start];
-      const int nexus_before = ws.runs[s + r].y;
+      const int pre_before = ws.runs[s + r].y;
       int body_start = 0, body_len = 0;
       if (kind == kNexus) {  // the grammar puts the owning body run right before
         body_start = ws.runs[s + r - 1].x;
         body_len = start - body_start;
       }
+      unsigned long long my_cost = 0;
       for (int j = 0; j < nt; ++j) {
         TileDesc d;
         d.req = b;
         d.p0 = start + j * kTileRows;
         d.nrows = min(kTileRows, end - d.p0);
-        if (kind == kSystem) {
-          d.r0_end = d.p0;
-          d.nx = 0;
-          d.r1_start = 0;
-          d.r1_len = 0;
+        d.pad = 0;
+        if (kind == kSystem) {          // system rows before the block, then the block
+          d.npre = d.p0;
+          d.seg_start = d.p0;
+          d.seg_len = d.nrows;
           d.ndiag = d.nrows;
-        } else if (kind == kText) {
-          d.r0_end = S;
-          d.nx = nexus_before;
-          d.r1_start = start;
-          d.r1_len = d.p0 - start;
+        } else if (kind == kText) {     // system + earlier Nexus, own body up to the block
+          d.npre = pre_before;
+          d.seg_start = start;
+          d.seg_len = d.p0 + d.nrows - start;
           d.ndiag = d.nrows;
-        } else if (kind == kNexus) {
-          d.r0_end = S;
-          d.nx = k_tot;
-          d.r1_start = body_start;
-          d.r1_len = body_len;
+        } else if (kind == kNexus) {    // system + every Nexus, the owning body
+          d.npre = npre_all;
+          d.seg_start = body_start;
+          d.seg_len = body_len;
           d.ndiag = 0;
-        } else {
-          d.r0_end = S;
-          d.nx = k_tot;
-          d.r1_start = start;
-          d.r1_len = d.p0 - start;
+        } else {                        // system + every Nexus, current query up to the block
+          d.npre = npre_all;
+          d.seg_start = start;
+          d.seg_len = d.p0 + d.nrows - start;
           d.ndiag = d.nrows;
         }
         ws.tiles[s + tile_carry + toff + j] = d;
+        my_cost += static_cast<unsigned long long>(tile_cost(d));
       }
+      if (my_cost) atomicAdd(&s_cost, my_cost);
     }
     tile_carry += ttot;
   }
-  if (threadIdx.x == 0) ws.req[b] = ReqInfo{tile_carry, S, k_tot, nruns};
+  __syncthreads();
+  if (threadIdx.x == 0) ws.req[b] = ReqInfo{tile_carry, S, k_tot, nruns, static_cast<int64_t>(s_cost), 0};
 }
 
-// One workgroup: order all descriptors by cost (number of 64-key steps),
-// most expensive first, and reset the per-XCD work queues.
-__global__ __launch_bounds__(kPlanThreads) void plan_order_kernel(int batch, const int32_t *__restrict__ cu,
-                                                                  PrefillWs ws, const int32_t *status) {
+// One workgroup: rank the requests by decreasing cost (index order beyond
+// kRankMax requests), give each its first slot in `order`, reset the queues.
+constexpr int kRankMax = 1024;
+
+__global__ __launch_bounds__(kPlanThreads) void plan_rank_kernel(int batch, PrefillWs ws, const int32_t *status) {
+  __shared__ long long cost[kRankMax];
+  __shared__ int sorted[kRankMax];
+  __shared__ int lds[kPlanThreads / kWave + 1];
+  __shared__ int s_ok;
+  const bool ok = block_status_clear(status, &s_ok);
+  const bool ranked = batch <= kRankMax;
+  if (ranked) {
+    for (int b = threadIdx.x; b < batch; b += kPlanThreads) cost[b] = ws.req[b].cost;
+    __syncthreads();
+    for (int b = threadIdx.x; b < batch; b += kPlanThreads) {
+      const long long c = cost[b];
+      int rank = 0;
+      for (int j = 0; j < batch; ++j) rank += (cost[j] > c || (cost[j] == c && j < b)) ? 1 : 0;
+      sorted[rank] = b;
+    }
+    __syncthreads();
+  }
+  int carry = 0;
+  for (int base = 0; base < batch; base += kPlanThreads) {
+    const int i = base + threadIdx.x;
+    const int b = i < batch ? (ranked ? sorted[i] : i) : 0;
+    const int n = i < batch ? ws.req[b].ntiles : 0;
+    int tot;
+    const int off = block_int_scan<kPlanThreads>(n, &tot, lds);
+    if (i < batch) ws.req_off[b] = carry + off;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) ws.ctrl[0] = ok ? carry : 0;
+  if (threadIdx.x < kNumXcd) ws.ctrl[8 + threadIdx.x] = 0;
+}
+
+// One workgroup per request: its descriptors by decreasing cost (a histogram
+// sort over kCostBuckets cost values, larger costs share the last bucket).
+__global__ __launch_bounds__(kPlanThreads) void plan_order_kernel(const int32_t *__restrict__ cu, PrefillWs ws,
+                                                                  const int32_t *status) {
   __shared__ int hist[kCostBuckets];
   __shared__ int lds[kPlanThreads / kWave + 1];
   __shared__ int s_ok;
   static_assert(kCostBuckets == kPlanThreads, "one histogram bucket per thread");
+  const int b = blockIdx.x;
   hist[threadIdx.x] = 0;
-  const bool ok = block_status_clear(status, &s_ok);
-  if (ok) {
-    for (int b = 0; b < batch; ++b) {
-      const int nt = ws.req[b].ntiles;
-      const int base = cu[b];
-      for (int j = threadIdx.x; j < nt; j += kPlanThreads) {
-        const int c = min(tile_cost(ws.tiles[base + j]), kCostBuckets - 1);
-        atomicAdd(&hist[kCostBuckets - 1 - c], 1);
-      }
-    }
+  if (!block_status_clear(status, &s_ok)) return;
+  const int nt = ws.req[b].ntiles;
+  const int base = cu[b];
+  const int dst = ws.req_off[b];
+  for (int j = threadIdx.x; j < nt; j += kPlanThreads) {
+    const int c = min(tile_cost(ws.tiles[base + j]), kCostBuckets - 1);
+    atomicAdd(&hist[kCostBuckets - 1 - c], 1);
   }
   __syncthreads();
   int total;
   const int off = block_int_scan<kPlanThreads>(hist[threadIdx.x], &total, lds);
   hist[threadIdx.x] = off;
   __syncthreads();
-  if (ok) {
-    for (int b = 0; b < batch; ++b) {
-      const int nt = ws.req[b].ntiles;
-      const int base = cu[b];
-      for (int j = threadIdx.x; j < nt; j += kPlanThreads) {
-        const int c = min(tile_cost(ws.tiles[base + j]), kCostBuckets - 1);
-        const int pos = atomicAdd(&hist[kCostBuckets - 1 - c], 1);
-        ws.order[pos] = base + j;
-      }
-    }
+  for (int j = threadIdx.x; j < nt; j += kPlanThreads) {
+    const int c = min(tile_cost(ws.tiles[base + j]), kCostBuckets - 1);
+    const int pos = atomicAdd(&hist[kCostBuckets - 1 - c], 1);
+    ws.order[dst + pos] = base + j;
   }
-  if (threadIdx.x == 0) ws.ctrl[0] = ok ? total : 0;
-  if (threadIdx.x < kNumXcd) ws.ctrl[8 + threadIdx.x] = 0;
 }
 
-hipError_t launch_plan(int batch, int total_tokens, const int32_t *cu, const uint8_t *role, const int32_t *turn,
-                       PrefillWs ws, int32_t *status, hipStream_t stream) {
+// Prefix copies: row j < S + K_tot of request b's prefix gets the K and V rows
+// of position prefix_pos[cu[b] + j].  One thread per 16-byte piece, pieces of a
+// row contiguous; the request of a row is found by bisection of cu.
+constexpr int kGatherThreads = 256;
+
+__global__ __launch_bounds__(kGatherThreads) void gather_prefix_kernel(int batch, const int32_t *__restrict__ cu,
+                                                                      const uint16_t *__restrict__ k,
+                                                                      const uint16_t *__restrict__ v, PrefillWs ws,
+                                                                      int row_pieces, long long total_pieces,
+                                                                      const int32_t *status) {
+  __shared__ int s_ok;
+  if (!block_status_clear(status, &s_ok)) return;
+  const long long stride = static_cast<long long>(gridDim.x) * kGatherThreads;
+  for (long long u = static_cast<long long>(blockIdx.x) * kGatherThreads + threadIdx.x; u < total_pieces;
+       u += stride) {
+    const int g = static_cast<int>(u / row_pieces);
+    const int c = static_cast<int>(u % row_pieces);
+    int lo = 0, hi = batch - 1;        // last b with cu[b] <= g
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (cu[mid] <= g) lo = mid; else hi = mid - 1;
+    }
+    const int j = g - cu[lo];
+    const ReqInfo ri = ws.req[lo];
+    if (j < 0 || j >= ri.system + ri.nexus_total) continue;
+    const size_t src = (static_cast<size_t>(cu[lo]) + ws.prefix_pos[g]) * row_pieces + c;
+    const size_t dst = static_cast<size_t>(g) * row_pieces + c;
+    reinterpret_cast<u32x4 *>(ws.k_pre)[dst] = reinterpret_cast<const u32x4 *>(k)[src];
+    reinterpret_cast<u32x4 *>(ws.v_pre)[dst] = reinterpret_cast<const u32x4 *>(v)[src];
+  }
+}
+
+hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus, const int32_t *cu,
+                       const uint8_t *role, const int32_t *turn, const uint16_t *k, const uint16_t *v, PrefillWs ws,
+                       int32_t *status, hipStream_t stream) {
   plan_runs_kernel<<<dim3(batch), dim3(kPlanThreads), 0, stream>>>(cu, role, turn, ws, total_tokens, status);
-  plan_order_kernel<<<dim3(1), dim3(kPlanThreads), 0, stream>>>(batch, cu, ws, status);
+  plan_rank_kernel<<<dim3(1), dim3(kPlanThreads), 0, stream>>>(batch, ws, status);
+  plan_order_kernel<<<dim3(batch), dim3(kPlanThreads), 0, stream>>>(cu, ws, status);
+  const int row_pieces = Hkv * D / 8;
+  const long long total = static_cast<long long>(total_tokens) * row_pieces;
+  long long want = (total + kGatherThreads - 1) / kGatherThreads;
+  const long long cap = static_cast<long long>(num_cus) * 8;
+  const int grid = static_cast<int>(want < cap ? (want > 0 ? want : 1) : cap);
+  gather_prefix_kernel<<<dim3(grid), dim3(kGatherThreads), 0, stream>>>(batch, cu, k, v, ws, row_pieces, total,
+                                                                        status);
   return hipGetLastError();
 }
 

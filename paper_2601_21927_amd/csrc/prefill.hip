@@ -25,10 +25,14 @@
 // max is updated lazily: O and the sum are rescaled only when the max grows by
 // more than 2^8, so most steps skip the rescale (p stays below 2^8).
 //
+// Keys come from two contiguous pieces (see TileDesc): the request's prefix copy
+// (system prompt, then its Nexus tokens, copied by the planner) and one range of
+// the request itself, so every load address is arithmetic on the descriptor.
+//
 // The grid is persistent: workgroup w serves the queue of XCD (w mod 8); item i
-// belongs to queue i mod 8, and items are ordered so that one queue sees one
-// kv-head (Hkv = 8) or a fixed subset of kv-heads, which keeps the K/V a queue
-// streams inside one XCD's L2.  Queues are filled most-expensive-first.
+// (descriptor slot i / Hkv, kv-head i mod Hkv) belongs to queue i mod 8.  Slots
+// run request by request, so the workgroups of one XCD work on one request at a
+// time and the K/V rows its blocks share stay in that XCD's L2.
 #include "common.h"
 
 namespace sonic {
@@ -40,15 +44,6 @@ namespace sonic {
 __device__ __forceinline__ int perm32(int m) { return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1); }
 
 __device__ __forceinline__ int acc_key(int v, int g) { return v < 8 ? 8 * g + v : 16 + 8 * g + (v - 8); }
-
-__device__ __forceinline__ int virtual_to_pos(const TileDesc &t, const int32_t *__restrict__ npos, int vk) {
-  if (vk < t.r0_end) return vk;
-  vk -= t.r0_end;
-  if (vk < t.nx) return npos[vk];
-  vk -= t.nx;
-  if (vk < t.r1_len) return t.r1_start + vk;
-  return t.p0 + (vk - t.r1_len);
-}
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) const void global_void_t;
@@ -70,6 +65,41 @@ template <int D> __device__ __forceinline__ int swz_v(int r) {
   return D == 128 ? ((4 * (r & 3)) ^ (2 * ((r >> 1) & 1))) : (2 * (r & 3));
 }
 
+// One 64-key step of one tensor into LDS, straight from global memory (no
+// registers), one 16-byte chunk per lane: the lane that fills (row m, slot s)
+// fetches chunk s ^ swizzle(m).  K row m holds key perm32(m) (MFMA row order);
+// V row r holds key r.  Virtual key vk < npre is row vk of the prefix copy, any
+// other is request position vk + seg_shift.  Keys past the list end repeat its
+// first key: their scores are masked, so they contribute exactly zero.  Wave w
+// issues instructions w, w + G, ... of the INSTS the step needs.
+template <int D, int G, bool IS_V>
+__device__ __forceinline__ void stage_tensor(uint16_t *lds_buf, const uint16_t *pre_base, const uint16_t *req_base,
+                                             size_t tok_stride, int wave, int lane, int c, int nv, int npre,
+                                             int seg_shift) {
+  constexpr int DC = D / 8;
+  constexpr int ROWS_PER_INST = kWave / DC;
+  constexpr int INSTS = kKeyChunk / ROWS_PER_INST;
+  constexpr int NJ = (INSTS + G - 1) / G;
+#pragma unroll
+  for (int jj = 0; jj < NJ; ++jj) {
+    const int ii = wave + jj * G;
+    if (ii < INSTS) {
+      const int m = ii * ROWS_PER_INST + lane / DC;
+      const int r = IS_V ? m : ((m & 32) | perm32(m & 31));
+      int vk = c * kKeyChunk + r;
+      if (vk >= nv) vk = 0;
+      const bool pre = vk < npre;
+      const int row = pre ? vk : vk + seg_shift;
+      const uint16_t *tb = pre ? pre_base : req_base;
+      const int src_chunk = (lane % DC) ^ (IS_V ? swz_v<D>(m) : swz_k<D>(m));
+      const uint16_t *src = tb + static_cast<size_t>(row) * tok_stride + src_chunk * 8;
+      // C-style casts: these change address spaces, which reinterpret_cast cannot do
+      __builtin_amdgcn_global_load_lds((global_void_t *)src, (lds_void_t *)(lds_buf + ii * ROWS_PER_INST * D), 16,
+                                       0, 0);
+    }
+  }
+}
+
 template <int D, int G>
 __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__restrict__ cu,
                                                                const uint16_t *__restrict__ q,
@@ -79,15 +109,18 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
   constexpr int DC = D / 8;              // 16-byte chunks per K/V row
   constexpr int DS = D / 16;             // d steps of the S product
   constexpr int DB = D / 32;             // 32-wide d blocks of the output
-  constexpr int ROWS_PER_INST = kWave / DC;        // rows filled by one direct-to-LDS wave instruction
-  constexpr int INSTS = kKeyChunk / ROWS_PER_INST;  // such instructions per tensor per 64-key step
   constexpr float kLazy = 8.f;           // rescale only when the running max grows by > 2^8
-  __shared__ __align__(16) uint16_t k_lds[2][kKeyChunk * D];   // [buf][64 keys][D], MFMA row order
-  __shared__ __align__(16) uint16_t v_lds[2][kKeyChunk * D];   // [buf][64 keys][D], key order
+  // Two buffers per tensor, as distinct arrays: the compiler then knows that the
+  // direct-to-LDS loads into one buffer cannot alias reads of the other and does
+  // not wait for them before those reads.
+  __shared__ __align__(16) uint16_t k_lds0[kKeyChunk * D];   // [64 keys][D], MFMA row order
+  __shared__ __align__(16) uint16_t k_lds1[kKeyChunk * D];
+  __shared__ __align__(16) uint16_t v_lds0[kKeyChunk * D];   // [64 keys][D], key order
+  __shared__ __align__(16) uint16_t v_lds1[kKeyChunk * D];
   __shared__ int s_item;
 
   const int Hq = Hkv * G;
-  const int wave = threadIdx.x / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);   // uniform: lets waves branch on it
   const int lane = threadIdx.x % kWave;
   const int n = lane & 31;
   const int g = lane >> 5;
@@ -111,34 +144,21 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
     const int kvh = item % Hkv;
     const TileDesc t = ws.tiles[slot];
     const int base = cu[t.req];
-    const int32_t *npos = ws.nexus_pos + base;
     const int h = kvh * G + wave;
     const int nv = tile_key_count(t);
     const int nF = nv - t.ndiag;
-    const uint16_t *kh = k + static_cast<size_t>(kvh) * D;
-    const uint16_t *vh = v + static_cast<size_t>(kvh) * D;
+    const int npre = t.npre;
+    const int seg_shift = t.seg_start - npre;    // request position of virtual key vk >= npre
     const size_t tok_stride = static_cast<size_t>(Hkv) * D;
+    const size_t head0 = static_cast<size_t>(base) * tok_stride + static_cast<size_t>(kvh) * D;
+    const uint16_t *kreq = k + head0;             // row 0 of the request, this kv-head
+    const uint16_t *vreq = v + head0;
+    const uint16_t *kpre = ws.k_pre + head0;      // row 0 of the request's prefix copy
+    const uint16_t *vpre = ws.v_pre + head0;
 
-    // Both tensors go straight to LDS, one 16-byte chunk per lane: the lane that fills
-    // (row m, slot s) fetches chunk s ^ swizzle(m).  K row m holds key perm32(m) (MFMA
-    // row order); V row r holds key r.  Keys past the list end repeat its first key:
-    // their scores are masked, so they contribute exactly zero.
-    auto stage = [&](int c, int buf) {
-      for (int i = wave; i < 2 * INSTS; i += G) {
-        const bool is_v = i >= INSTS;
-        const int ii = is_v ? i - INSTS : i;
-        const int m = ii * ROWS_PER_INST + lane / DC;
-        const int cslot = lane % DC;
-        const int r = is_v ? m : ((m & 32) | perm32(m & 31));
-        int vk = c * kKeyChunk + r;
-        if (vk >= nv) vk = 0;
-        const int p = virtual_to_pos(t, npos, vk);
-        const int src_chunk = cslot ^ (is_v ? swz_v<D>(m) : swz_k<D>(m));
-        const uint16_t *src = (is_v ? vh : kh) + static_cast<size_t>(base + p) * tok_stride + src_chunk * 8;
-        uint16_t *dst = is_v ? &v_lds[buf][ii * ROWS_PER_INST * D] : &k_lds[buf][ii * ROWS_PER_INST * D];
-        // C-style casts: these change address spaces, which reinterpret_cast cannot do
-        __builtin_amdgcn_global_load_lds((global_void_t *)src, (lds_void_t *)dst, 16, 0, 0);
-      }
+    auto stage = [&](int c, uint16_t *kb_lds, uint16_t *vb_lds) {
+      stage_tensor<D, G, false>(kb_lds, kpre, kreq, tok_stride, wave, lane, c, nv, npre, seg_shift);
+      stage_tensor<D, G, true>(vb_lds, vpre, vreq, tok_stride, wave, lane, c, nv, npre, seg_shift);
     };
 
     // Q^T fragments (B operand of S): lane (row n, half g) holds d = 16*ds + 8*g .. +7.
@@ -161,13 +181,10 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
     float l_run = 0.f;
 
     const int nchunks = (nv + kKeyChunk - 1) / kKeyChunk;
-    stage(0, 0);
-    wait_vmem();
-    __syncthreads();
-
-    for (int c = 0; c < nchunks; ++c) {
-      const int cur = c & 1;
-      if (c + 1 < nchunks) stage(c + 1, cur ^ 1);   // next step streams into the other buffer
+    // One 64-key step: compute on (kc_lds, vc_lds) while step c + 1 streams into
+    // (kn_lds, vn_lds).
+    auto step = [&](int c, const uint16_t *kc_lds, const uint16_t *vc_lds, uint16_t *kn_lds, uint16_t *vn_lds) {
+      if (c + 1 < nchunks) stage(c + 1, kn_lds, vn_lds);
       const int vk0 = c * kKeyChunk;
 
       // ---- S^T = K . Q^T for two 32-key blocks ----
@@ -179,7 +196,7 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
 #pragma unroll
         for (int ds = 0; ds < DS; ++ds) {
           const bf16x8 a =
-              *reinterpret_cast<const bf16x8 *>(&k_lds[cur][(m * DC + ((2 * ds + g) ^ swz_k<D>(m))) * 8]);
+              *reinterpret_cast<const bf16x8 *>(&kc_lds[(m * DC + ((2 * ds + g) ^ swz_k<D>(m))) * 8]);
           sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ds], sacc[kb], 0, 0, 0);
         }
       }
@@ -237,7 +254,7 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
           for (int hh = 0; hh < 2; ++hh) {
             const int r = 16 * ks + 4 * hh + v_row_off;
             const int chunk = (dd >> 3) ^ swz_v<D>(r);
-            const uint16_t *pa = &v_lds[cur][r * D + chunk * 8 + (dd & 4)];
+            const uint16_t *pa = &vc_lds[r * D + chunk * 8 + (dd & 4)];
             part[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)pa);
           }
           const u32x4 w = {__builtin_bit_cast(uint2, part[0]).x, __builtin_bit_cast(uint2, part[0]).y,
@@ -248,6 +265,15 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
       }
       wait_vmem();
       __syncthreads();
+    };
+
+    stage(0, k_lds0, v_lds0);
+    wait_vmem();
+    __syncthreads();
+    for (int c = 0; c < nchunks; c += 2) {
+      step(c, k_lds0, v_lds0, k_lds1, v_lds1);
+      if (c + 1 >= nchunks) break;
+      step(c + 1, k_lds1, v_lds1, k_lds0, v_lds0);
     }
 
     // ---- normalise and store: lane (n, g) holds d = 32*db + 8*i + 4*g + (0..3) ----

@@ -55,7 +55,7 @@ class SonicBatch:
         self.Hq = 0 if self.q is None else self.q.shape[1]
         self.out = None if self.q is None else torch.empty((self.T, self.Hq, self.d), dtype=torch.float32,
                                                            device=self.device)
-        ws = sonic.prefill_workspace_bytes(self.batch, self.total_tokens)
+        ws = sonic.prefill_workspace_bytes(self.batch, self.total_tokens, self.Hkv, self.d)
         self.prefill_ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=self.device)
         self.cache = None
 

@@ -61,7 +61,7 @@ def lib() -> ctypes.CDLL:
     L.sonic_layout_stats_host.restype = _i32
     L.sonic_layout_stats_host.argtypes = [_i32, _p, _p, _p, _p, _p]
     L.sonic_prefill_workspace_bytes.restype = _sz
-    L.sonic_prefill_workspace_bytes.argtypes = [_i32, _i32]
+    L.sonic_prefill_workspace_bytes.argtypes = [_i32, _i32, _i32, _i32]
     L.sonic_segment_attn_prefill.restype = _i32
     L.sonic_segment_attn_prefill.argtypes = [_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _f32, _p, _p,
                                              _sz, _p, _p]
@@ -135,8 +135,8 @@ def layout_stats_host(cu_seqlens, role, turn_id):
 
 
 # ----------------------------------------------------------------- step 1: prefill
-def prefill_workspace_bytes(batch: int, total_tokens: int) -> int:
-    return int(lib().sonic_prefill_workspace_bytes(batch, total_tokens))
+def prefill_workspace_bytes(batch: int, total_tokens: int, num_kv_heads: int, head_dim: int) -> int:
+    return int(lib().sonic_prefill_workspace_bytes(batch, total_tokens, num_kv_heads, head_dim))
 
 
 def segment_attn_prefill(cu_seqlens, role, turn_id, q, k, v, out, workspace, dev_status, softmax_scale=None,
