@@ -134,6 +134,8 @@ size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens, int32_
  *                         256-byte aligned; contents need no initialisation
  *   dev_status            device int32 (see conventions); SONIC_ERR_BAD_LAYOUT
  *                         is reported here and then no output is written
+ * Returns SONIC_ERR_UNSUPPORTED when T * Hkv * d * 2 bytes (one of k, v) reach
+ * 4 GiB or T * Hq * d reaches 2^40.
  */
 int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t num_q_heads,
                                    int32_t num_kv_heads, int32_t head_dim, const int32_t *cu_seqlens,

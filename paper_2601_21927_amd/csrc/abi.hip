@@ -246,6 +246,8 @@ int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t 
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) || !aligned(workspace, 256))
     return SONIC_ERR_INVALID_ARG;
   if (static_cast<size_t>(total_tokens) * Hq * d >= (size_t(1) << 40)) return SONIC_ERR_UNSUPPORTED;
+  // K/V rows are addressed with 32-bit byte offsets inside one request
+  if (static_cast<size_t>(total_tokens) * Hkv * d * 2 >= (size_t(1) << 32)) return SONIC_ERR_UNSUPPORTED;
   PrefillWs ws;
   const size_t need = prefill_ws_layout(batch, total_tokens, Hkv, d, &ws, static_cast<char *>(workspace));
   if (workspace_bytes < need) return SONIC_ERR_WORKSPACE;

@@ -113,25 +113,40 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_kernel(
   const int rq = lane / DCH;   // value phase: row slot
 
   // Rows below len come from the cache; row len is the new token (its inputs, not the
-  // cache, so no split depends on split 0's append).
+  // cache, so no split depends on split 0's append).  Loads are unconditional: a row
+  // past the split's end reads row r_begin instead and is masked out of the softmax,
+  // so the compiler can wait for each group's loads alone (a conditional load would
+  // make it wait for all of them).
+  auto row_ptr = [&](int r, const uint16_t *cache_base, const uint16_t *fresh) {
+    const int rr = r < r_end ? r : r_begin;
+    return rr < len ? cache_base + static_cast<size_t>(rr) * row_stride : fresh;
+  };
   auto load_k = [&](int r0, u32x4 (&kr)[KS]) {
-    const int r = r0 + (lane & 15);
-    const uint16_t *krow = (r < len) ? kbase + static_cast<size_t>(r) * row_stride : knew;
-    const bool ok = r < r_end;
+    const uint16_t *krow = row_ptr(r0 + (lane & 15), kbase, knew);
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      kr[ks] = u32x4{0u, 0u, 0u, 0u};
-      if (ok) kr[ks] = *reinterpret_cast<const u32x4 *>(krow + 32 * ks + 8 * quarter);
-    }
+    for (int ks = 0; ks < KS; ++ks) kr[ks] = *reinterpret_cast<const u32x4 *>(krow + 32 * ks + 8 * quarter);
   };
   auto load_v = [&](int r0, u32x4 (&vr)[VPL]) {
 #pragma unroll
     for (int i = 0; i < VPL; ++i) {
-      const int r = r0 + rq + i * ROWQ;
-      const uint16_t *vrow = (r < len) ? vbase + static_cast<size_t>(r) * row_stride : vnew;
-      vr[i] = u32x4{0u, 0u, 0u, 0u};
-      if (r < r_end) vr[i] = *reinterpret_cast<const u32x4 *>(vrow + 8 * dc);
+      const uint16_t *vrow = row_ptr(r0 + rq + i * ROWQ, vbase, vnew);
+      vr[i] = *reinterpret_cast<const u32x4 *>(vrow + 8 * dc);
     }
+  };
+  // masked full-cache mode: the role bytes of this lane's four score rows r0 + 4*quarter + i
+  auto load_roles = [&](int r0) {
+    uint32_t roles = 0;
+    if (row_role != nullptr) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = r0 + 4 * quarter + i;
+        // rows at or past len are the new token (role CURRENT); the clamped index keeps
+        // the load inside the request's rows
+        const uint32_t rb = row_role[base + max(0, min(r, len - 1))];
+        roles |= (r >= len ? static_cast<uint32_t>(kCurrent) : rb) << (8 * i);
+      }
+    }
+    return roles;
   };
 
   float acc[G][8];
@@ -147,11 +162,13 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_kernel(
   // kGroups x (K + V) rows in flight instead of waiting one memory round trip per group.
   for (int rb = r_begin; rb < r_end; rb += kRoundRows) {
     u32x4 kr[kGroups][KS], vr[kGroups][VPL];
+    uint32_t roles[kGroups];
 #pragma unroll
     for (int j = 0; j < kGroups; ++j) {
       const int r0 = rb + (j * kDecWaves + wave) * kDecRowsPerGroup;
       load_k(r0, kr[j]);
       load_v(r0, vr[j]);
+      roles[j] = load_roles(r0);
     }
 #pragma unroll
     for (int j = 0; j < kGroups; ++j) {
@@ -167,9 +184,7 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_kernel(
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = r0 + 4 * quarter + i;
-        bool vis = r < r_end;
-        // (the clamped index keeps the role load inside the request's rows even when unused)
-        if (row_role != nullptr) vis = vis && (r >= len || row_role[base + max(0, min(r, len - 1))] != kText);
+        const bool vis = r < r_end && ((roles[j] >> (8 * i)) & 0xFF) != kText;
         x[i] = vis ? sacc[i] * scale_log2 : -INFINITY;
         mloc = fmaxf(mloc, x[i]);
       }
@@ -282,19 +297,15 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_kernel(
 }
 
 // Merge the split partials of one (kv-head, request); kv-head 0 advances the length.
-// The split maxima and sums are staged in LDS first, so every global load of the
-// merge is independent of the others.
-constexpr int kMaxSplits = 128;
-
+// Every thread owns output elements (q-head, d) and loads, for a batch of up to
+// eight splits at once, the split's max, sum and accumulator of its element, so a
+// batch costs one memory round trip; batches are merged online.
 template <int D, int G>
 __global__ __launch_bounds__(kDecThreads) void decode_combine_kernel(int32_t *__restrict__ cache_len,
                                                                      float *__restrict__ out, DecodeWs ws, int Hkv,
                                                                      int nsplit_max) {
   constexpr int REC = G * (D + 2);
-  __shared__ float m_s[kMaxSplits][G];
-  __shared__ float w_s[kMaxSplits][G];   // weight of each split: exp2(m_s - M) / L
-  __shared__ float M_s[G];
-  __shared__ float L_s[G];
+  constexpr int BATCH = 8;
   const int kvh = blockIdx.x;
   const int b = blockIdx.y;
   const int pair = b * Hkv + kvh;
@@ -302,47 +313,40 @@ __global__ __launch_bounds__(kDecThreads) void decode_combine_kernel(int32_t *__
   // every record of the launch is valid (unused splits wrote empty ones), so the split
   // count and the records are fetched together
   const int nsp = ws.nsplit[b];
-  for (int t = threadIdx.x; t < nsplit_max * G; t += kDecThreads) {
-    const int sp = t / G, hh = t % G;
-    m_s[sp][hh] = recs[sp * REC + hh * (D + 2)];
-    w_s[sp][hh] = recs[sp * REC + hh * (D + 2) + 1];   // the split's sum, for now
-  }
-  if (nsp == 0) return;   // the request could not append this step (uniform per block)
-  if (kvh == 0 && threadIdx.x == 0) cache_len[b] += 1;   // nothing else reads it in this kernel
-  if (nsp == 1) return;   // the split kernel wrote the output itself
-  __syncthreads();
-  if (threadIdx.x < G) {
-    const int hh = threadIdx.x;
-    float M = -INFINITY;
-    for (int sp = 0; sp < nsplit_max; ++sp) M = fmaxf(M, m_s[sp][hh]);
-    float L = 0.f;
-    for (int sp = 0; sp < nsplit_max; ++sp)
-      L += (m_s[sp][hh] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_s[sp][hh] - M)) * w_s[sp][hh];
-    M_s[hh] = M;
-    L_s[hh] = L;
-  }
-  __syncthreads();
-  for (int t = threadIdx.x; t < nsplit_max * G; t += kDecThreads) {
-    const int sp = t / G, hh = t % G;
-    w_s[sp][hh] = (m_s[sp][hh] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_s[sp][hh] - M_s[hh]) / L_s[hh];
-  }
-  __syncthreads();
   float *orow = out + (static_cast<size_t>(b) * Hkv * G + kvh * G) * D;
   for (int idx = threadIdx.x; idx < G * D; idx += kDecThreads) {
     const int hh = idx / D, dd = idx % D;
-    const float *col = recs + hh * (D + 2) + 2 + dd;
-    float A = 0.f;
-    int sp = 0;
-    for (; sp + 8 <= nsplit_max; sp += 8) {   // eight independent loads in flight
-      float a[8];
+    float M = -INFINITY, L = 0.f, A = 0.f;
+    for (int sp0 = 0; sp0 < nsplit_max; sp0 += BATCH) {
+      float m[BATCH], l[BATCH], a[BATCH];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) a[u] = col[(sp + u) * REC];
+      for (int u = 0; u < BATCH; ++u) {
+        const int sp = min(sp0 + u, nsplit_max - 1);   // a repeated record is weighted 0 below
+        const float *r = recs + static_cast<size_t>(sp) * REC + hh * (D + 2);
+        m[u] = r[0];
+        l[u] = r[1];
+        a[u] = r[2 + dd];
+      }
+      float Mb = M;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) A += w_s[sp + u][hh] * a[u];
+      for (int u = 0; u < BATCH; ++u)
+        if (sp0 + u < nsplit_max) Mb = fmaxf(Mb, m[u]);
+      if (Mb == -INFINITY) continue;
+      const float c = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mb);
+      L *= c;
+      A *= c;
+#pragma unroll
+      for (int u = 0; u < BATCH; ++u) {
+        const float w = (sp0 + u < nsplit_max && m[u] != -INFINITY) ? __builtin_amdgcn_exp2f(m[u] - Mb) : 0.f;
+        L = fmaf(w, l[u], L);
+        A = fmaf(w, a[u], A);
+      }
+      M = Mb;
     }
-    for (; sp < nsplit_max; ++sp) A += w_s[sp][hh] * col[sp * REC];
-    orow[idx] = A;
+    if (nsp > 1) orow[idx] = A / L;   // nsp == 1: the split kernel wrote the output itself
   }
+  // nsp == 0: the request could not append this step and keeps its length
+  if (nsp > 0 && kvh == 0 && threadIdx.x == 0) cache_len[b] += 1;   // nothing else reads it here
 }
 
 int decode_num_splits(int max_ctx, int rows_per_split) { return (max_ctx + rows_per_split - 1) / rows_per_split; }

@@ -50,8 +50,39 @@ typedef __attribute__((address_space(1))) const void global_void_t;
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
 
-// s_waitcnt with vmcnt(0) and the other counters left at their maximum (gfx9 encoding).
-__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// s_waitcnt vmcnt(N), the other counters left at their maximum (gfx9 encoding):
+// wait until at most N of this wave's vector-memory operations are outstanding.
+// They complete in issue order, so this waits for all but the N most recent.
+template <int N> __device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier for the LDS pipeline.  __syncthreads() would also wait for
+// every outstanding vector-memory operation (its release fence covers the
+// direct-to-LDS loads still in flight), which would drain the prefetch; here the
+// loads a step needs are waited for explicitly with wait_vm, this wave's LDS
+// reads are completed (lgkmcnt(0)) before it arrives, and the signal fences keep
+// the compiler from moving memory operations across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));   // lgkmcnt(0)
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// One direct-to-LDS load: every lane fetches 16 bytes from its global address
+// and the wave writes them to LDS at dst + 16 * lane (dst is wave-uniform, passed
+// in M0).  Written as inline assembly so that the compiler does not track it as a
+// pending LDS write: it would otherwise wait for every such load, including the
+// prefetches into the other buffers, before each LDS read.  Completion is waited
+// for explicitly (wait_vm) before the data is read.
+__device__ __forceinline__ void dma_row16(const char *src, const uint16_t *dst) {
+  // C-style cast: converting the LDS pointer to its 32-bit address
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
+      reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) uint16_t *)dst)));
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds) : "memory", "m0");
+}
 
 // LDS bank swizzles (XOR on the 16-byte chunk index of a row), chosen so that the
 // reads below are conflict-free whether a pass covers 16 lanes of 32 banks or
@@ -70,11 +101,12 @@ template <int D> __device__ __forceinline__ int swz_v(int r) {
 // fetches chunk s ^ swizzle(m).  K row m holds key perm32(m) (MFMA row order);
 // V row r holds key r.  Virtual key vk < npre is row vk of the prefix copy, any
 // other is request position vk + seg_shift.  Keys past the list end repeat its
-// first key: their scores are masked, so they contribute exactly zero.  Wave w
-// issues instructions w, w + G, ... of the INSTS the step needs.
+// first key: their scores are masked, so they contribute exactly zero (a step
+// wholly past the end loads key 0 throughout and is never read).  Wave w issues
+// instructions w, w + G, ... of the INSTS the step needs.
 template <int D, int G, bool IS_V>
-__device__ __forceinline__ void stage_tensor(uint16_t *lds_buf, const uint16_t *pre_base, const uint16_t *req_base,
-                                             size_t tok_stride, int wave, int lane, int c, int nv, int npre,
+__device__ __forceinline__ void stage_tensor(uint16_t *lds_buf, const char *pre_base, const char *req_base,
+                                             uint32_t row_bytes, int wave, int lane, int c, int nv, int npre,
                                              int seg_shift) {
   constexpr int DC = D / 8;
   constexpr int ROWS_PER_INST = kWave / DC;
@@ -82,20 +114,19 @@ __device__ __forceinline__ void stage_tensor(uint16_t *lds_buf, const uint16_t *
   constexpr int NJ = (INSTS + G - 1) / G;
 #pragma unroll
   for (int jj = 0; jj < NJ; ++jj) {
-    const int ii = wave + jj * G;
-    if (ii < INSTS) {
+    // Every wave issues exactly NJ instructions (so that its wait counts are
+    // static); where G does not divide INSTS, the surplus ones repeat the last
+    // instruction, writing the same bytes to the same LDS rows.
+    const int ii = min(wave + jj * G, INSTS - 1);
+    {
       const int m = ii * ROWS_PER_INST + lane / DC;
       const int r = IS_V ? m : ((m & 32) | perm32(m & 31));
       int vk = c * kKeyChunk + r;
       if (vk >= nv) vk = 0;
       const bool pre = vk < npre;
-      const int row = pre ? vk : vk + seg_shift;
-      const uint16_t *tb = pre ? pre_base : req_base;
-      const int src_chunk = (lane % DC) ^ (IS_V ? swz_v<D>(m) : swz_k<D>(m));
-      const uint16_t *src = tb + static_cast<size_t>(row) * tok_stride + src_chunk * 8;
-      // C-style casts: these change address spaces, which reinterpret_cast cannot do
-      __builtin_amdgcn_global_load_lds((global_void_t *)src, (lds_void_t *)(lds_buf + ii * ROWS_PER_INST * D), 16,
-                                       0, 0);
+      const uint32_t chunk_bytes = static_cast<uint32_t>(((lane % DC) ^ (IS_V ? swz_v<D>(m) : swz_k<D>(m))) * 16);
+      const uint32_t off = static_cast<uint32_t>(pre ? vk : vk + seg_shift) * row_bytes + chunk_bytes;
+      dma_row16(pre ? pre_base + off : req_base + off, lds_buf + ii * ROWS_PER_INST * D);
     }
   }
 }
@@ -151,14 +182,19 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
     const int seg_shift = t.seg_start - npre;    // request position of virtual key vk >= npre
     const size_t tok_stride = static_cast<size_t>(Hkv) * D;
     const size_t head0 = static_cast<size_t>(base) * tok_stride + static_cast<size_t>(kvh) * D;
-    const uint16_t *kreq = k + head0;             // row 0 of the request, this kv-head
-    const uint16_t *vreq = v + head0;
-    const uint16_t *kpre = ws.k_pre + head0;      // row 0 of the request's prefix copy
-    const uint16_t *vpre = ws.v_pre + head0;
+    // row 0 of the request (and of its prefix copy) for this kv-head; rows are
+    // row_bytes apart, and every row of a request lies below 4 GiB from its row 0
+    const char *kreq = reinterpret_cast<const char *>(k + head0);
+    const char *vreq = reinterpret_cast<const char *>(v + head0);
+    const char *kpre = reinterpret_cast<const char *>(ws.k_pre + head0);
+    const char *vpre = reinterpret_cast<const char *>(ws.v_pre + head0);
+    const uint32_t row_bytes = static_cast<uint32_t>(tok_stride * 2);
 
-    auto stage = [&](int c, uint16_t *kb_lds, uint16_t *vb_lds) {
-      stage_tensor<D, G, false>(kb_lds, kpre, kreq, tok_stride, wave, lane, c, nv, npre, seg_shift);
-      stage_tensor<D, G, true>(vb_lds, vpre, vreq, tok_stride, wave, lane, c, nv, npre, seg_shift);
+    auto stage_k = [&](int c, uint16_t *buf) {
+      stage_tensor<D, G, false>(buf, kpre, kreq, row_bytes, wave, lane, c, nv, npre, seg_shift);
+    };
+    auto stage_v = [&](int c, uint16_t *buf) {
+      stage_tensor<D, G, true>(buf, vpre, vreq, row_bytes, wave, lane, c, nv, npre, seg_shift);
     };
 
     // Q^T fragments (B operand of S): lane (row n, half g) holds d = 16*ds + 8*g .. +7.
@@ -183,8 +219,21 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
     const int nchunks = (nv + kKeyChunk - 1) / kKeyChunk;
     // One 64-key step: compute on (kc_lds, vc_lds) while step c + 1 streams into
     // (kn_lds, vn_lds).
-    auto step = [&](int c, const uint16_t *kc_lds, const uint16_t *vc_lds, uint16_t *kn_lds, uint16_t *vn_lds) {
-      if (c + 1 < nchunks) stage(c + 1, kn_lds, vn_lds);
+    // Pipeline, per wave: K of step c + 2 is requested as soon as every wave has
+    // finished S(c), V of step c + 1 as soon as every wave has finished P.V(c - 1).
+    // Each wave issues exactly NJ direct-to-LDS instructions per tensor and step,
+    // in the order K(0) V(0) K(1) | V(1) K(2) | V(2) K(3) | ..., also for steps past
+    // the end of the key list (those load key 0 and are never read).  So at the start
+    // of step c the loads newer than K(c) are V(c) and K(c+1), and in its middle the
+    // loads newer than V(c) are K(c+1) and V(c+1): both waits are "all but the 2 * NJ
+    // most recent", the same at every step.
+    constexpr int NJ = ((kKeyChunk / (kWave / (D / 8))) + G - 1) / G;
+    static_assert(2 * NJ < 64, "the wait count fits vmcnt");
+    __builtin_assume(wave < G);
+    auto step = [&](int c, uint16_t *kc_lds, const uint16_t *vc_lds, uint16_t *vn_lds) {
+      wait_vm<2 * NJ>();
+      lds_barrier();                                   // K(c) in LDS; every wave is past P.V(c - 1)
+      stage_v(c + 1, vn_lds);
       const int vk0 = c * kKeyChunk;
 
       // ---- S^T = K . Q^T for two 32-key blocks ----
@@ -201,6 +250,9 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
         }
       }
 
+      wait_vm<2 * NJ>();
+      lds_barrier();                                   // V(c) in LDS; every wave is past S(c)
+      stage_k(c + 2, kc_lds);
       // ---- mask (ragged end / causal diagonal only), online softmax ----
       if (vk0 + kKeyChunk > nF) {
         // Row n sees every key before the diagonal block and diagonal keys j <= n:
@@ -263,17 +315,16 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
                                                              0, 0);
         }
       }
-      wait_vmem();
-      __syncthreads();
     };
 
-    stage(0, k_lds0, v_lds0);
-    wait_vmem();
-    __syncthreads();
-    for (int c = 0; c < nchunks; c += 2) {
-      step(c, k_lds0, v_lds0, k_lds1, v_lds1);
+    stage_k(0, k_lds0);
+    stage_v(0, v_lds0);
+    stage_k(1, k_lds1);
+    step(0, k_lds0, v_lds0, v_lds1);
+    for (int c = 1; c < nchunks; c += 2) {
+      step(c, k_lds1, v_lds1, v_lds0);
       if (c + 1 >= nchunks) break;
-      step(c + 1, k_lds1, v_lds1, k_lds0, v_lds0);
+      step(c + 1, k_lds0, v_lds0, v_lds1);
     }
 
     // ---- normalise and store: lane (n, g) holds d = 32*db + 8*i + 4*g + (0..3) ----
