@@ -230,7 +230,7 @@ def main():
         ach = per_launch / (dc_ms * 1e-3 / steps_dec) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": measured_traffic("decode"),
-                "kernel": "sonic_compressed_decode, one call (decode_kernel + decode_combine_kernel)"}
+                "kernel": "sonic_compressed_decode, one call (decode_kernel)"}
     else:
         roof = {"bound": "hbm", "achieved": round(compact_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(compact_gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic("compact"),

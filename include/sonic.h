@@ -189,8 +189,9 @@ size_t sonic_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t 
  * over the request's rows 0 .. cache_len[b] (the appended row included): a
  * generated token belongs to the current turn, so it sees every retained row.
  * cache_len[b] is incremented on the device, so a decode loop needs no host
- * round trip.  Two kernels: split-K partials over the context, then a
- * log-sum-exp merge that also advances cache_len.
+ * round trip.  One kernel: the context of each (request, kv-head) is split over
+ * up to ~256 / (B * Hkv) workgroups, and the split that finishes last merges
+ * the partials by log-sum-exp.
  *
  * With row_role == NULL the cache is a compact one and every row is visible.
  * With row_role != NULL (device uint8 [rows], indexed like cache rows) the
@@ -201,7 +202,8 @@ size_t sonic_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t 
  *   q              device bf16 [B][Hq][d];  k_new, v_new: device bf16 [B][Hkv][d]
  *   out            device fp32 [B][Hq][d]
  *   workspace      device, 256-byte aligned, >= sonic_decode_workspace_bytes(B, Hq, d,
- *                  max_ctx); contents need no initialisation
+ *                  max_ctx); zero-filled before its first use (it holds completion
+ *                  counters that every call leaves at zero again)
  *   dev_status     SONIC_ERR_CAPACITY when cache_len[b] + 1 exceeds the capacity
  *                  or max_ctx: request b is then left unchanged (no append, no
  *                  output, same length) while the other requests proceed.  Unlike

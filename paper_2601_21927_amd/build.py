@@ -26,6 +26,9 @@ ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-variable",
+    # M0 is declared clobbered by the direct-to-LDS inline assembly on purpose; the
+    # build checks that no compiler-generated code uses it (_check_m0_only_in_asm)
+    "-Wno-inline-asm",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
 PACKED_FP32 = re.compile(r"\bv_pk_(fma|mul|add)_f32\b")
@@ -56,12 +59,32 @@ def _check_no_packed_fp32():
         raise RuntimeError("packed-FP32 instructions in device code:\n" + "\n".join(bad[:20]))
 
 
+def _check_m0_only_in_asm():
+    """The direct-to-LDS loads set M0 inside inline assembly that declares it
+    clobbered; the compiler does not preserve a reserved register across such a
+    statement, so no compiler-generated code may rely on M0 anywhere."""
+    bad = []
+    for s in glob.glob(os.path.join(BUILD, "*-hip-amdgcn-amd-amdhsa-*.s")):
+        in_asm = False
+        with open(s) as f:
+            for ln, line in enumerate(f, 1):
+                if ";;#ASMSTART" in line:
+                    in_asm = True
+                elif ";;#ASMEND" in line:
+                    in_asm = False
+                elif not in_asm and re.search(r"\bm0\b", line.split(";", 1)[0]):
+                    bad.append(f"{os.path.basename(s)}:{ln}: {line.strip()}")
+    if bad:
+        raise RuntimeError("compiler-generated code uses M0:\n" + "\n".join(bad[:20]))
+
+
 def build(verbose: bool = True) -> str:
     os.makedirs(BUILD, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
     with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
         objs = list(ex.map(_compile, srcs))
     _check_no_packed_fp32()
+    _check_m0_only_in_asm()
     tmp = LIB + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)

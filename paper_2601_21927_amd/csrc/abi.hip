@@ -20,8 +20,8 @@ hipError_t launch_compact(int batch, int total_tokens, int max_seqlen, int Hkv, 
                           const uint16_t *k, const uint16_t *v, uint16_t *kc, uint16_t *vc, const int64_t *row_off,
                           const int32_t *row_cap, int32_t *cache_len, int32_t *keep_idx, int32_t *status,
                           hipStream_t stream);
-int decode_num_splits(int max_ctx, int rows_per_split);
-hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int rows_per_split, uint16_t *kc,
+int decode_splits(int batch, int Hkv, int max_ctx);
+hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int nsplit, uint16_t *kc,
                          uint16_t *vc, const int64_t *row_off, const int32_t *row_cap, int32_t *cache_len,
                          const uint8_t *row_role, const uint16_t *q, const uint16_t *k_new, const uint16_t *v_new,
                          float scale_log2, float *out, void *ws, int32_t *status, hipStream_t stream);
@@ -289,24 +289,18 @@ int32_t sonic_kv_compact(int32_t batch, int32_t total_tokens, int32_t max_seqlen
 }
 
 // ---------------------------------------------------------------- decode
-static int decode_rows_per_split(int32_t max_ctx) {
-  // rounds of 256 rows; more than one round per split only when that keeps the split
-  // count within what the merge stages in LDS (128)
-  constexpr long kRound = 256, kMaxSplits = 128;
-  long rounds = (static_cast<long>(max_ctx) + kRound * kMaxSplits - 1) / (kRound * kMaxSplits);
-  if (rounds < 1) rounds = 1;
-  return static_cast<int>(rounds * kRound);
-}
-
 static size_t decode_ws_bytes(int32_t batch, int32_t Hq, int32_t d, int32_t nsplit) {
-  const size_t counts = align_up(static_cast<size_t>(batch) * sizeof(int32_t), 256);
-  return counts + static_cast<size_t>(batch) * Hq * nsplit * (d + 2) * sizeof(float);
+  // counters: per request, then per (request, kv-head) with Hkv <= Hq
+  const size_t counters = align_up(static_cast<size_t>(batch) * sizeof(int32_t), 256) +
+                          align_up(static_cast<size_t>(batch) * Hq * sizeof(int32_t), 256);
+  const size_t records = nsplit > 1 ? static_cast<size_t>(batch) * Hq * nsplit * (d + 2) * sizeof(float) : 0;
+  return counters + records;
 }
 
 size_t sonic_decode_workspace_bytes(int32_t batch, int32_t Hq, int32_t d, int32_t max_ctx) {
   if (batch <= 0 || Hq <= 0 || max_ctx <= 0) return 256;
-  // enough for any kv-head count: the smallest split size bounds the split count
-  return align_up(decode_ws_bytes(batch, Hq, d, decode_num_splits(max_ctx, decode_rows_per_split(max_ctx))), 256);
+  // enough for any kv-head count: one kv-head gives the most splits
+  return align_up(decode_ws_bytes(batch, Hq, d, decode_splits(batch, 1, max_ctx)), 256);
 }
 
 int32_t sonic_compressed_decode(int32_t batch, int32_t Hq, int32_t Hkv, int32_t d, int32_t max_ctx, void *k_cache,
@@ -328,9 +322,9 @@ int32_t sonic_compressed_decode(int32_t batch, int32_t Hq, int32_t Hkv, int32_t 
   if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(q, 16) || !aligned(k_new, 16) ||
       !aligned(v_new, 16) || !aligned(out, 16) || !aligned(workspace, 256))
     return SONIC_ERR_INVALID_ARG;
-  const int rps = decode_rows_per_split(max_ctx);
-  if (workspace_bytes < decode_ws_bytes(batch, Hq, d, decode_num_splits(max_ctx, rps))) return SONIC_ERR_WORKSPACE;
-  hipError_t e = launch_decode(batch, Hq, Hkv, d, max_ctx, rps, static_cast<uint16_t *>(k_cache),
+  const int nsplit = decode_splits(batch, Hkv, max_ctx);
+  if (workspace_bytes < decode_ws_bytes(batch, Hq, d, nsplit)) return SONIC_ERR_WORKSPACE;
+  hipError_t e = launch_decode(batch, Hq, Hkv, d, max_ctx, nsplit, static_cast<uint16_t *>(k_cache),
                                static_cast<uint16_t *>(v_cache), cache_row_off, cache_row_cap, cache_len, row_role,
                                static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k_new),
                                static_cast<const uint16_t *>(v_new), static_cast<float>(softmax_scale * kLog2e), out,

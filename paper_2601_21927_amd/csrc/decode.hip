@@ -1,58 +1,99 @@
-// Decode over the retained context {I_sys, N, Q_n} (App. C, Eq.(15)).
+// Decode over the retained context {I_sys, N, Q_n} (problem statement).
 //
-// decode_kernel: grid (split, kv-head, request), 4 waves.  A
-// split owns rows [split*R, split*R + R) of the request's context rows 0..len
-// (row len is the token being generated: it is read from k_new/v_new, and split 0
-// of each kv-head also appends it to the cache).  A split is processed in rounds
-// of 256 rows; each wave issues the loads of all four of its 16-row groups of a
-// round before working through them:
-//   scores    S^T (16 rows x 16 cols) = K . Q^T with v_mfma_f32_16x16x32_bf16;
-//             column c < G is q-head kvh*G + c, the other columns are zero;
-//   softmax   per q-head, online, fp32, exp2 with log2(e) folded into the scale;
-//   values    P . V on the vector ALUs in fp32: lane (d chunk, row slot)
-//             accumulates 8 d-values of every q-head of the group.
-// The four waves merge through LDS.  With one split the workgroup writes the
-// output; otherwise it stores its partial (max, sum, acc) for decode_combine.
+// decode_kernel: grid (split, kv-head, request), 8 waves.  A split owns a
+// contiguous range of the request's context rows 0..len (row len is the token
+// being generated: it is read from k_new/v_new, and split 0 of each kv-head also
+// appends it to the cache).  The range is cut into 16-row groups, dealt to the
+// waves round-robin; per group a wave computes
+//   scores   S^T (16 rows x 16 cols) = K . Q^T   v_mfma_f32_16x16x32_bf16;
+//            column c < G is q-head kvh*G + c;
+//   softmax  per q-head, online, fp32, exp2 with log2(e) folded into the scale;
+//            a column's statistics live in the four lanes that hold it;
+//   values   O^T (d x 16 cols) += V^T . P^T   v_mfma_f32_16x16x16_bf16, V read
+//            back transposed (ds_read_b64_tr_b16); P^T is the score accumulator
+//            itself, rounded to bf16 (its lane layout is the operand layout).
+// K and V rows go straight from global memory to a two-slot LDS ring of the
+// wave's own (direct-to-LDS loads), so a wave keeps its next group in flight
+// while it computes one.  The waves then merge through LDS.
 //
-// decode_combine_kernel: grid (kv-head, request) merges the splits with the
-// log-sum-exp rule and (kv-head 0) advances cache_len.  Cross-workgroup merging
-// is left to a second kernel on purpose: the L2 caches of the eight XCDs are
-// not coherent with each other, so an in-kernel hand-off needs device-scope
-// fences that write back and invalidate a whole L2, evicting the K/V that
-// other workgroups are streaming; the kernel boundary gives the same
-// visibility for free.
+// With one split the workgroup writes the output.  With several, each split
+// stores its partial (max, sum, acc) and counts itself done with an atomic; the
+// split that arrives last merges the partials by log-sum-exp and writes the
+// output.  The eight XCDs' L2 caches are not coherent with each other, so the
+// hand-off does not go through them: the partials are stored write-through at
+// system scope and read back with loads that bypass the caches, which needs no
+// L2 writeback or invalidate (either would evict the K/V other workgroups are
+// streaming).  Finally the last pair of a request to finish advances cache_len:
+// by then every workgroup of the request has read the old length.
 #include "common.h"
 
 namespace sonic {
 
-constexpr int kDecThreads = 256;
-constexpr int kDecWaves = kDecThreads / kWave;
-constexpr int kDecRowsPerGroup = 16;
-constexpr int kGroups = 4;                                           // groups per wave per round
-constexpr int kRoundRows = kGroups * kDecWaves * kDecRowsPerGroup;  // 256 rows per round
+constexpr int kDecWaves = 8;
+constexpr int kDecThreads = kDecWaves * kWave;
+constexpr int kGroupRows = 16;
 
+// Device workspace of the decode; the counters are zero between calls.
 struct DecodeWs {
+  int32_t *done;      // [B]      kv-heads of request b finished in this call
+  int32_t *arrive;    // [B*Hkv]  splits of a (request, kv-head) finished in this call
   float *part;        // [B*Hkv][nsplit][G*(D+2)] partial (m[G], l[G], acc[G][D]) per split
-  int32_t *nsplit;    // [B] splits used by request b in this step (0: request skipped)
 };
 
-template <int D, int G>
-__global__ __launch_bounds__(kDecThreads, 2) void decode_kernel(
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+// The K/V loads of the pipeline go straight to LDS and are written as inline
+// assembly, so the compiler does not count them (it would otherwise wait for the
+// prefetched group as well before reading the current one); their completion is
+// waited for explicitly (wait_vm).
+// 16 bytes per lane into LDS at dst + 16 * lane (dst wave-uniform, passed in M0)
+__device__ __forceinline__ void dma16(const void *src, const uint16_t *dst) {
+  // C-style cast: converting the LDS pointer to its 32-bit address
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
+      reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) uint16_t *)dst)));
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds) : "memory", "m0");
+}
+// A load that bypasses the (non-coherent) caches, for partials another XCD stored
+// write-through; completion is waited for explicitly.
+__device__ __forceinline__ float load_sys(const float *p) {
+  float v;
+  asm volatile("global_load_dword %0, %1, off sc0 sc1" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+// s_waitcnt vmcnt(N), other counters at their maximum (gfx9 encoding)
+template <int N> __device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <int D, int G, bool MASKED>
+__global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
     uint16_t *__restrict__ kc, uint16_t *__restrict__ vc, const int64_t *__restrict__ row_off,
     const int32_t *__restrict__ row_cap, int32_t *__restrict__ cache_len, const uint8_t *__restrict__ row_role,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k_new, const uint16_t *__restrict__ v_new,
-    float *__restrict__ out, DecodeWs ws, int32_t *status, int Hkv, int rows_per_split, int nsplit_max, int max_ctx,
+    float *__restrict__ out, DecodeWs ws, int32_t *status, int Hkv, int nsplit_max, int max_ctx,
     float scale_log2) {
-  constexpr int KS = D / 32;            // k steps of the 16x16x32 product
-  constexpr int DCH = D / 8;            // 8-value d chunks per row
-  constexpr int ROWQ = kWave / DCH;     // row slots of the value phase
-  constexpr int VPL = kDecRowsPerGroup / ROWQ;   // V rows per lane per group
-  constexpr int REC = G * (D + 2);      // floats of one partial record
-  __shared__ float p_lds[kDecWaves][kDecRowsPerGroup][8];
-  __shared__ float corr_lds[kDecWaves][8];
-  __shared__ float m_lds[kDecWaves][8];
-  __shared__ float l_lds[kDecWaves][8];
-  __shared__ float acc_lds[kDecWaves][G][D];
+  constexpr int KS = D / 32;                   // k steps of the 16x16x32 score product
+  constexpr int DB = D / 16;                   // 16-wide d blocks of the value product
+  constexpr int DC = D / 8;                    // 16-byte chunks per row
+  constexpr int NI = kGroupRows * DC / kWave;  // direct-to-LDS instructions per tensor and group
+  constexpr int NG = 2 * NI;                   // loads per lane per group
+  constexpr int REC = G * (D + 2);             // floats of one partial record
+  constexpr int SLOT = kGroupRows * D;         // elements of one tensor's slot
+  constexpr int KSWZ = DC - 1;                 // K: 16-byte chunk p of row r at p ^ (r & KSWZ)
+  constexpr int VSWZ = DC / 2 - 1;             // V: 32-byte segment s of row r at s ^ (r & VSWZ)
+  static_assert(NI * kWave == kGroupRows * DC, "a group's rows are whole DMA instructions");
+  // ring: [wave][slot 0/1][K, V][16 rows][D] with the swizzles above (K for the
+  // row-fragment reads of the scores, V for the transposing reads); reused for the
+  // merge of the waves at the end
+  __shared__ __align__(16) uint16_t ring[kDecWaves * 2 * 2 * SLOT];
+  __shared__ float m_lds[kDecWaves][16];
+  __shared__ float l_lds[kDecWaves][16];
+  __shared__ int s_last;
+  static_assert(sizeof(float) * kDecWaves * G * D <= sizeof(uint16_t) * kDecWaves * 4 * SLOT,
+                "the merge fits in the ring");
 
   const int split = blockIdx.x;
   const int kvh = blockIdx.y;
@@ -61,331 +102,303 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_kernel(
   const int len = cache_len[b];
   const int n_ctx = len + 1;
   if (n_ctx > row_cap[b] || n_ctx > max_ctx) {   // uniform over the request: no append, no output
-    if (split == 0 && kvh == 0 && threadIdx.x == 0) {
-      raise_status(status, SONIC_ERR_CAPACITY);
-      ws.nsplit[b] = 0;
-    }
+    if (split == 0 && kvh == 0 && threadIdx.x == 0) raise_status(status, SONIC_ERR_CAPACITY);
     return;
   }
-  const int nsp = (n_ctx + rows_per_split - 1) / rows_per_split;
-  if (split == 0 && kvh == 0 && threadIdx.x == 0) ws.nsplit[b] = nsp;
-  if (split >= nsp) {
-    // an unused split leaves an empty record (max -inf, sum 0, acc 0) so that the merge can
-    // read every record without first waiting for the split count
-    if (nsp > 1) {
-      float *rec = ws.part + (static_cast<size_t>(b * Hkv + kvh) * nsplit_max + split) * REC;
-      for (int idx = threadIdx.x; idx < REC; idx += kDecThreads) rec[idx] = (idx % (D + 2) == 0) ? -INFINITY : 0.f;
-    }
-    return;
-  }
-  const int r_begin = split * rows_per_split;
-  const int r_end = min(n_ctx, r_begin + rows_per_split);
+  // split ranges: R rows each, a multiple of the group size
+  const int R = ((n_ctx + nsplit_max - 1) / nsplit_max + kGroupRows - 1) / kGroupRows * kGroupRows;
+  const int nsp = (n_ctx + R - 1) / R;   // splits that hold rows; the others have nothing to do
+  if (split >= nsp) return;
+  const int r_begin = split * R;
+  const int r_end = min(n_ctx, r_begin + R);
+  const int ngroups = (r_end - r_begin + kGroupRows - 1) / kGroupRows;
+  const int iters = (ngroups + kDecWaves - 1) / kDecWaves;   // the same for every wave
   const int64_t base = row_off[b];
-  const int wave = threadIdx.x / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = threadIdx.x % kWave;
+  const int col = lane & 15;       // score column (q-head) / value-product column
+  const int quarter = lane >> 4;   // score rows 4*quarter .. +3
   const size_t row_stride = static_cast<size_t>(Hkv) * D;
   const uint16_t *knew = k_new + (static_cast<size_t>(b) * Hkv + kvh) * D;
   const uint16_t *vnew = v_new + (static_cast<size_t>(b) * Hkv + kvh) * D;
   uint16_t *kbase = kc + static_cast<size_t>(base) * row_stride + static_cast<size_t>(kvh) * D;
   uint16_t *vbase = vc + static_cast<size_t>(base) * row_stride + static_cast<size_t>(kvh) * D;
 
-  if (split == 0 && threadIdx.x < DCH) {   // append the new token at row len
+  if (split == 0 && threadIdx.x < DC) {   // append the new token at row len
     const size_t dst = static_cast<size_t>(len) * row_stride + threadIdx.x * 8;
     *reinterpret_cast<u32x4 *>(kbase + dst) = reinterpret_cast<const u32x4 *>(knew)[threadIdx.x];
     *reinterpret_cast<u32x4 *>(vbase + dst) = reinterpret_cast<const u32x4 *>(vnew)[threadIdx.x];
   }
 
-  // Q^T fragments (B operand): lane (col = lane%16, quarter = lane/16) holds
-  // d = 32*ks + 8*quarter .. +7 of q-head kvh*G + col (zero for col >= G).
-  const int col = lane & 15;
-  const int quarter = lane >> 4;
+  // Q^T fragments (B operand of the scores): lane (col, quarter) holds d = 32*ks +
+  // 8*quarter .. +7 of q-head kvh*G + col (columns col >= G load head kvh*G and are
+  // never read back).
   bf16x8 qf[KS];
   {
-    const uint16_t *qrow = q + (static_cast<size_t>(b) * Hq + kvh * G + col) * D;
+    const uint16_t *qrow = q + (static_cast<size_t>(b) * Hq + kvh * G + (col < G ? col : 0)) * D;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      u32x4 w = {0u, 0u, 0u, 0u};
-      if (col < G) w = *reinterpret_cast<const u32x4 *>(qrow + 32 * ks + 8 * quarter);
-      qf[ks] = __builtin_bit_cast(bf16x8, w);
-    }
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const bf16x8 *>(qrow + 32 * ks + 8 * quarter);
   }
-  const int dc = lane % DCH;   // value phase: d chunk
-  const int rq = lane / DCH;   // value phase: row slot
 
-  // Rows below len come from the cache; row len is the new token (its inputs, not the
-  // cache, so no split depends on split 0's append).  Loads are unconditional: a row
-  // past the split's end reads row r_begin instead and is masked out of the softmax,
-  // so the compiler can wait for each group's loads alone (a conditional load would
-  // make it wait for all of them).
-  auto row_ptr = [&](int r, const uint16_t *cache_base, const uint16_t *fresh) {
-    const int rr = r < r_end ? r : r_begin;
-    return rr < len ? cache_base + static_cast<size_t>(rr) * row_stride : fresh;
-  };
-  auto load_k = [&](int r0, u32x4 (&kr)[KS]) {
-    const uint16_t *krow = row_ptr(r0 + (lane & 15), kbase, knew);
+  // Row r of the context: the cache below len, the new token at len.  Rows past the
+  // split's end load row r_begin instead (and are masked), so every group issues the
+  // same loads and the waits can be counted.
+  auto row_of = [&](int r) { return r < r_end ? r : r_begin; };
+  auto kptr = [&](int r) { return r < len ? kbase + static_cast<size_t>(r) * row_stride : knew; };
+  auto vptr = [&](int r) { return r < len ? vbase + static_cast<size_t>(r) * row_stride : vnew; };
+  uint16_t *my_ring = ring + wave * 4 * SLOT;
+
+  // group j of this wave covers rows r_begin + 16 * (wave + j * kDecWaves) ...
+  auto group_row0 = [&](int j) { return r_begin + kGroupRows * (wave + j * kDecWaves); };
+  // issue the loads of group j into ring slot s: lane -> (row, 16-byte position) of
+  // each instruction's rows; the position holds the row's swizzled chunk
+  auto issue = [&](int j, int s) {
+    const int r0 = group_row0(j);
+    uint16_t *kslot = my_ring + s * 2 * SLOT;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kr[ks] = *reinterpret_cast<const u32x4 *>(krow + 32 * ks + 8 * quarter);
-  };
-  auto load_v = [&](int r0, u32x4 (&vr)[VPL]) {
-#pragma unroll
-    for (int i = 0; i < VPL; ++i) {
-      const uint16_t *vrow = row_ptr(r0 + rq + i * ROWQ, vbase, vnew);
-      vr[i] = *reinterpret_cast<const u32x4 *>(vrow + 8 * dc);
+    for (int i = 0; i < NI; ++i) {
+      const int rl = (i * kWave + lane) / DC;
+      const int pos = (i * kWave + lane) % DC;
+      const int r = row_of(r0 + rl);
+      dma16(kptr(r) + (pos ^ (rl & KSWZ)) * 8, kslot + i * kWave * 8);
+      dma16(vptr(r) + (pos ^ (2 * (rl & VSWZ))) * 8, kslot + SLOT + i * kWave * 8);
     }
   };
-  // masked full-cache mode: the role bytes of this lane's four score rows r0 + 4*quarter + i
+  // masked full-cache mode: the role bytes of this lane's four score rows
   auto load_roles = [&](int r0) {
     uint32_t roles = 0;
-    if (row_role != nullptr) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = r0 + 4 * quarter + i;
-        // rows at or past len are the new token (role CURRENT); the clamped index keeps
-        // the load inside the request's rows
-        const uint32_t rb = row_role[base + max(0, min(r, len - 1))];
-        roles |= (r >= len ? static_cast<uint32_t>(kCurrent) : rb) << (8 * i);
-      }
+    for (int i = 0; i < 4; ++i) {
+      // the clamped index keeps the load inside the request's rows; rows at or past
+      // len are the new token, whose role is CURRENT (see the mask below)
+      const int r = r0 + 4 * quarter + i;
+      roles |= static_cast<uint32_t>(row_role[base + max(0, min(r, len - 1))]) << (8 * i);
     }
     return roles;
   };
 
-  float acc[G][8];
+  f32x4 oacc[DB];
 #pragma unroll
-  for (int hh = 0; hh < G; ++hh)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[hh][e] = 0.f;
-  float m_run = -INFINITY;
-  float l_run = 0.f;
+  for (int i = 0; i < DB; ++i) oacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY;   // running max (log2 domain) of column col, lagging by at most 8
+  float l_run = 0.f;         // this lane's share of the column's sum
 
-  // A round covers kRoundRows rows: wave w takes 16-row groups j*4 + w, j < kGroups.  All
-  // of a round's loads are issued before any of its groups is processed, so a wave keeps
-  // kGroups x (K + V) rows in flight instead of waiting one memory round trip per group.
-  for (int rb = r_begin; rb < r_end; rb += kRoundRows) {
-    u32x4 kr[kGroups][KS], vr[kGroups][VPL];
-    uint32_t roles[kGroups];
+  // score fragments: lane (col, quarter) reads row col, d = 32*ks + 8*quarter (chunk 4*ks + quarter)
+  const int k_off = col * D;
+  // transposed-read geometry (value product): 16-lane group kq reads rows 4*kq + (t >> 2)
+  // at d = 16*db + 4*(t & 3), t = lane % 16; lane t then holds V[4*kq .. +3][16*db + t]
+  const int tr_row = 4 * quarter + (col >> 2);
+  const int tr_off = tr_row * D + 4 * (col & 3);
+  const int tr_swz = tr_row & VSWZ;
+
+  auto process = [&](int j, int s) {
+    const int r0 = group_row0(j);
+    const uint16_t *kslot = my_ring + s * 2 * SLOT;
+    const uint32_t roles = MASKED ? load_roles(r0) : 0u;
+    f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < kGroups; ++j) {
-      const int r0 = rb + (j * kDecWaves + wave) * kDecRowsPerGroup;
-      load_k(r0, kr[j]);
-      load_v(r0, vr[j]);
-      roles[j] = load_roles(r0);
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8 *>(kslot + k_off + (((4 * ks + quarter) ^ (col & KSWZ)) * 8));
+      sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[ks], sacc, 0, 0, 0);
     }
+    // lane (col, quarter) holds rows r0 + 4*quarter + i of column col
+    float x[4];
+    float mloc = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < kGroups; ++j) {
-      const int r0 = rb + (j * kDecWaves + wave) * kDecRowsPerGroup;
-      if (r0 >= r_end) break;   // uniform across the wave
-      f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[j][ks]), qf[ks], sacc, 0, 0, 0);
-      // lane (col, quarter) holds rows r0 + 4*quarter + i, i = 0..3, of head col
-      float x[4];
-      float mloc = -INFINITY;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = r0 + 4 * quarter + i;
-        const bool vis = r < r_end && ((roles[j] >> (8 * i)) & 0xFF) != kText;
-        x[i] = vis ? sacc[i] * scale_log2 : -INFINITY;
-        mloc = fmaxf(mloc, x[i]);
-      }
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    for (int i = 0; i < 4; ++i) {
+      const int r = r0 + 4 * quarter + i;
+      bool vis = r < r_end;
+      if (MASKED) vis = vis && (r >= len || ((roles >> (8 * i)) & 0xFF) != kText);
+      x[i] = vis ? sacc[i] * scale_log2 : -INFINITY;
+      mloc = fmaxf(mloc, x[i]);
+    }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    if (__any(mloc > m_run + 8.f)) {   // rescale only when the max grows by more than 2^8
       const float m_new = fmaxf(m_run, mloc);
-      const float corr = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-      float psum = 0.f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float p = (m_new == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(x[i] - m_new);
-        psum += p;
-        if (col < 8) p_lds[wave][4 * quarter + i][col] = p;
-      }
+      const float corr = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
       m_run = m_new;
-      l_run = l_run * corr + psum;
-      if (quarter == 0 && col < 8) corr_lds[wave][col] = corr;
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
+      l_run *= corr;
 #pragma unroll
-      for (int hh = 0; hh < G; ++hh) {
-        const float c = corr_lds[wave][hh];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[hh][e] *= c;
-      }
-#pragma unroll
-      for (int i = 0; i < VPL; ++i) {
-        const int rr = rq + i * ROWQ;
-        float vv[8];
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          vv[2 * w] = bf16_lo(vr[j][i][w]);
-          vv[2 * w + 1] = bf16_hi(vr[j][i][w]);
-        }
-#pragma unroll
-        for (int hh = 0; hh < G; ++hh) {
-          const float p = p_lds[wave][rr][hh];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) acc[hh][e] = fmaf(p, vv[e], acc[hh][e]);
-        }
-      }
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      for (int i = 0; i < DB; ++i) oacc[i] *= corr;
     }
+    f32x4 p;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      p[i] = (x[i] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(x[i] - m_run);
+      l_run += p[i];
+    }
+    const v4i16 pb = __builtin_bit_cast(v4i16, __builtin_convertvector(p, bf16x4));
+    const uint16_t *vslot = kslot + SLOT;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const uint16_t *pa = vslot + tr_off + ((db ^ tr_swz) * 16);
+      // C-style cast: the transposing read takes an LDS-qualified pointer
+      const v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)pa);
+      oacc[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, pb, oacc[db], 0, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));   // lgkmcnt(0): slot s may be refilled
+  };
+
+  // two-deep pipeline: group j + 2 is issued as soon as group j has left its slot
+  issue(0, 0);
+  issue(1, 1);
+  for (int j = 0; j < iters; j += 2) {
+    wait_vm<NG>();                      // group j has landed (group j + 1 may not have)
+    process(j, 0);
+    issue(j + 2, 0);
+    if (j + 1 >= iters) break;
+    wait_vm<NG>();
+    process(j + 1, 1);
+    issue(j + 3, 1);
   }
+  wait_vm<0>();   // the trailing (unused) loads, before the ring is reused
 
-  // ---- merge row slots inside the wave, then the four waves through LDS ----
-#pragma unroll
-  for (int hh = 0; hh < G; ++hh)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float a = acc[hh][e];
-#pragma unroll
-      for (int o = DCH; o < kWave; o <<= 1) a += __shfl_xor(a, o);
-      acc[hh][e] = a;
-    }
+  // ---- merge: columns across the four quarters, then the waves through LDS ----
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
-  if (lane < DCH) {
-#pragma unroll
-    for (int hh = 0; hh < G; ++hh)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc_lds[wave][hh][8 * dc + e] = acc[hh][e];
-  }
-  if (quarter == 0 && col < 8) {
+  if (quarter == 0) {
     m_lds[wave][col] = m_run;
     l_lds[wave][col] = l_run;
+  }
+  __syncthreads();   // every wave is done with the ring
+  float *acc_lds = reinterpret_cast<float *>(ring);   // [wave][G][D]
+  if (col < G) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc_lds[(wave * G + col) * D + 16 * db + 4 * quarter + i] = oacc[db][i];
   }
   __syncthreads();
 
   const int pair = b * Hkv + kvh;
   float *orow = out + (static_cast<size_t>(b) * Hq + kvh * G) * D;
-  if (nsp == 1) {
-    for (int idx = threadIdx.x; idx < G * D; idx += kDecThreads) {
-      const int hh = idx / D, dd = idx % D;
-      float M = -INFINITY;
-#pragma unroll
-      for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, m_lds[w][hh]);
-      float L = 0.f, A = 0.f;
-#pragma unroll
-      for (int w = 0; w < kDecWaves; ++w) {
-        const float sc = (m_lds[w][hh] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_lds[w][hh] - M);
-        L += sc * l_lds[w][hh];
-        A += sc * acc_lds[w][hh][dd];
-      }
-      orow[idx] = A / L;
-    }
-    return;
-  }
   float *rec = ws.part + (static_cast<size_t>(pair) * nsplit_max + split) * REC;
-  for (int idx = threadIdx.x; idx < REC; idx += kDecThreads) {
-    const int hh = idx / (D + 2), f = idx % (D + 2);
+  for (int idx = threadIdx.x; idx < G * D; idx += kDecThreads) {
+    const int hh = idx / D, dd = idx % D;
     float M = -INFINITY;
 #pragma unroll
     for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, m_lds[w][hh]);
-    float val = M;
-    if (f > 0) {
-      val = 0.f;
+    float L = 0.f, A = 0.f;
 #pragma unroll
-      for (int w = 0; w < kDecWaves; ++w) {
-        const float sc = (m_lds[w][hh] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_lds[w][hh] - M);
-        val += sc * (f == 1 ? l_lds[w][hh] : acc_lds[w][hh][f - 2]);
-      }
+    for (int w = 0; w < kDecWaves; ++w) {
+      const float sc = (m_lds[w][hh] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_lds[w][hh] - M);
+      L = fmaf(sc, l_lds[w][hh], L);
+      A = fmaf(sc, acc_lds[(w * G + hh) * D + dd], A);
     }
-    rec[idx] = val;
+    if (nsp == 1) {
+      orow[idx] = A / L;
+    } else {   // write-through at system scope (see the top of the file)
+      if (dd == 0) {
+        __hip_atomic_store(rec + hh * (D + 2), M, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        __hip_atomic_store(rec + hh * (D + 2) + 1, L, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      }
+      __hip_atomic_store(rec + hh * (D + 2) + 2 + dd, A, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+  }
+  if (nsp > 1) {
+    wait_vm<0>();      // this thread's partial is stored
+    __syncthreads();   // ... and every thread's
+    if (threadIdx.x == 0) s_last = (atomicAdd(&ws.arrive[pair], 1) == nsp - 1);
+    __syncthreads();
+    if (!s_last) return;
+    // the last split merges every split's partial, a batch of eight per memory round trip
+    const float *recs = ws.part + static_cast<size_t>(pair) * nsplit_max * REC;
+    for (int idx = threadIdx.x; idx < G * D; idx += kDecThreads) {
+      const int hh = idx / D, dd = idx % D;
+      float M = -INFINITY, L = 0.f, A = 0.f;
+      for (int sp0 = 0; sp0 < nsp; sp0 += 8) {
+        float m[8], l[8], a[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const float *r = recs + static_cast<size_t>(min(sp0 + u, nsp - 1)) * REC + hh * (D + 2);
+          m[u] = load_sys(r);
+          l[u] = load_sys(r + 1);
+          a[u] = load_sys(r + 2 + dd);
+        }
+        wait_vm<0>();
+#pragma unroll
+        for (int u = 0; u < 8; ++u) asm volatile("" : "+v"(m[u]), "+v"(l[u]), "+v"(a[u]));
+        float Mb = M;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (sp0 + u < nsp) Mb = fmaxf(Mb, m[u]);
+        const float c = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mb);
+        L *= c;
+        A *= c;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const float w = (sp0 + u < nsp && m[u] != -INFINITY) ? __builtin_amdgcn_exp2f(m[u] - Mb) : 0.f;
+          L = fmaf(w, l[u], L);
+          A = fmaf(w, a[u], A);
+        }
+        M = Mb;
+      }
+      orow[idx] = A / L;
+    }
+    if (threadIdx.x == 0) ws.arrive[pair] = 0;
+  }
+  // the last kv-head of the request to finish advances the length: by then every
+  // workgroup of the request has read it
+  __syncthreads();
+  if (threadIdx.x == 0) s_last = (atomicAdd(&ws.done[b], 1) == Hkv - 1);
+  __syncthreads();
+  if (s_last && threadIdx.x == 0) {
+    cache_len[b] = n_ctx;
+    ws.done[b] = 0;
   }
 }
 
-// Merge the split partials of one (kv-head, request); kv-head 0 advances the length.
-// Every thread owns output elements (q-head, d) and loads, for a batch of up to
-// eight splits at once, the split's max, sum and accumulator of its element, so a
-// batch costs one memory round trip; batches are merged online.
-template <int D, int G>
-__global__ __launch_bounds__(kDecThreads) void decode_combine_kernel(int32_t *__restrict__ cache_len,
-                                                                     float *__restrict__ out, DecodeWs ws, int Hkv,
-                                                                     int nsplit_max) {
-  constexpr int REC = G * (D + 2);
-  constexpr int BATCH = 8;
-  const int kvh = blockIdx.x;
-  const int b = blockIdx.y;
-  const int pair = b * Hkv + kvh;
-  const float *recs = ws.part + static_cast<size_t>(pair) * nsplit_max * REC;
-  // every record of the launch is valid (unused splits wrote empty ones), so the split
-  // count and the records are fetched together
-  const int nsp = ws.nsplit[b];
-  float *orow = out + (static_cast<size_t>(b) * Hkv * G + kvh * G) * D;
-  for (int idx = threadIdx.x; idx < G * D; idx += kDecThreads) {
-    const int hh = idx / D, dd = idx % D;
-    float M = -INFINITY, L = 0.f, A = 0.f;
-    for (int sp0 = 0; sp0 < nsplit_max; sp0 += BATCH) {
-      float m[BATCH], l[BATCH], a[BATCH];
-#pragma unroll
-      for (int u = 0; u < BATCH; ++u) {
-        const int sp = min(sp0 + u, nsplit_max - 1);   // a repeated record is weighted 0 below
-        const float *r = recs + static_cast<size_t>(sp) * REC + hh * (D + 2);
-        m[u] = r[0];
-        l[u] = r[1];
-        a[u] = r[2 + dd];
-      }
-      float Mb = M;
-#pragma unroll
-      for (int u = 0; u < BATCH; ++u)
-        if (sp0 + u < nsplit_max) Mb = fmaxf(Mb, m[u]);
-      if (Mb == -INFINITY) continue;
-      const float c = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mb);
-      L *= c;
-      A *= c;
-#pragma unroll
-      for (int u = 0; u < BATCH; ++u) {
-        const float w = (sp0 + u < nsplit_max && m[u] != -INFINITY) ? __builtin_amdgcn_exp2f(m[u] - Mb) : 0.f;
-        L = fmaf(w, l[u], L);
-        A = fmaf(w, a[u], A);
-      }
-      M = Mb;
-    }
-    if (nsp > 1) orow[idx] = A / L;   // nsp == 1: the split kernel wrote the output itself
-  }
-  // nsp == 0: the request could not append this step and keeps its length
-  if (nsp > 0 && kvh == 0 && threadIdx.x == 0) cache_len[b] += 1;   // nothing else reads it here
+// Splits per (request, kv-head): about 256 workgroups (one per CU), each of at
+// least 256 rows; one split when there are that many pairs already.
+int decode_splits(int batch, int Hkv, int max_ctx) {
+  const long pairs = static_cast<long>(batch) * Hkv;
+  if (pairs >= 256) return 1;
+  long s = (256 + pairs - 1) / pairs;
+  const long by_rows = (static_cast<long>(max_ctx) + 255) / 256;
+  if (s > by_rows) s = by_rows;
+  return static_cast<int>(s < 1 ? 1 : s);
 }
-
-int decode_num_splits(int max_ctx, int rows_per_split) { return (max_ctx + rows_per_split - 1) / rows_per_split; }
 
 size_t decode_ws_layout(int batch, int Hkv, int G, int D, int nsplit, DecodeWs *ws, char *base) {
-  const size_t nbytes = (static_cast<size_t>(batch) * sizeof(int32_t) + 255) / 256 * 256;
-  const size_t pbytes = static_cast<size_t>(batch) * Hkv * nsplit * G * (D + 2) * sizeof(float);
+  const size_t dbytes = (static_cast<size_t>(batch) * sizeof(int32_t) + 255) / 256 * 256;
+  const size_t abytes = (static_cast<size_t>(batch) * Hkv * sizeof(int32_t) + 255) / 256 * 256;
+  const size_t pbytes = nsplit > 1 ? static_cast<size_t>(batch) * Hkv * nsplit * G * (D + 2) * sizeof(float) : 0;
   if (ws) {
-    ws->nsplit = reinterpret_cast<int32_t *>(base);
-    ws->part = reinterpret_cast<float *>(base + nbytes);
+    ws->done = reinterpret_cast<int32_t *>(base);
+    ws->arrive = reinterpret_cast<int32_t *>(base + dbytes);
+    ws->part = reinterpret_cast<float *>(base + dbytes + abytes);
   }
-  return nbytes + pbytes;
+  return dbytes + abytes + pbytes;
 }
 
 template <int D, int G>
-static void launch_decode_dg(dim3 grid, int batch, int Hkv, int max_ctx, int rows_per_split, int nsplit,
-                             uint16_t *kc, uint16_t *vc, const int64_t *row_off, const int32_t *row_cap,
-                             int32_t *cache_len, const uint8_t *row_role, const uint16_t *q, const uint16_t *k_new,
-                             const uint16_t *v_new, float scale_log2, float *out, DecodeWs ws, int32_t *status,
-                             hipStream_t stream) {
-  decode_kernel<D, G><<<grid, dim3(kDecThreads), 0, stream>>>(kc, vc, row_off, row_cap, cache_len, row_role, q, k_new,
-                                                              v_new, out, ws, status, Hkv, rows_per_split, nsplit,
-                                                              max_ctx, scale_log2);
-  decode_combine_kernel<D, G><<<dim3(Hkv, batch), dim3(kDecThreads), 0, stream>>>(cache_len, out, ws, Hkv, nsplit);
+static void launch_decode_dg(dim3 grid, int batch, int Hkv, int max_ctx, int nsplit, uint16_t *kc, uint16_t *vc,
+                             const int64_t *row_off, const int32_t *row_cap, int32_t *cache_len,
+                             const uint8_t *row_role, const uint16_t *q, const uint16_t *k_new, const uint16_t *v_new,
+                             float scale_log2, float *out, DecodeWs ws, int32_t *status, hipStream_t stream) {
+  if (row_role != nullptr)
+    decode_kernel<D, G, true><<<grid, dim3(kDecThreads), 0, stream>>>(kc, vc, row_off, row_cap, cache_len, row_role,
+                                                                      q, k_new, v_new, out, ws, status, Hkv, nsplit,
+                                                                      max_ctx, scale_log2);
+  else
+    decode_kernel<D, G, false><<<grid, dim3(kDecThreads), 0, stream>>>(kc, vc, row_off, row_cap, cache_len,
+                                                                       row_role, q, k_new, v_new, out, ws, status,
+                                                                       Hkv, nsplit, max_ctx, scale_log2);
 }
 
-hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int rows_per_split, uint16_t *kc,
-                         uint16_t *vc, const int64_t *row_off, const int32_t *row_cap, int32_t *cache_len,
-                         const uint8_t *row_role, const uint16_t *q, const uint16_t *k_new, const uint16_t *v_new,
-                         float scale_log2, float *out, void *ws_base, int32_t *status, hipStream_t stream) {
+hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int nsplit, uint16_t *kc, uint16_t *vc,
+                         const int64_t *row_off, const int32_t *row_cap, int32_t *cache_len, const uint8_t *row_role,
+                         const uint16_t *q, const uint16_t *k_new, const uint16_t *v_new, float scale_log2,
+                         float *out, void *ws_base, int32_t *status, hipStream_t stream) {
   const int G = Hq / Hkv;
-  const int nsplit = decode_num_splits(max_ctx, rows_per_split);
   DecodeWs ws;
   decode_ws_layout(batch, Hkv, G, D, nsplit, &ws, static_cast<char *>(ws_base));
   dim3 grid(nsplit, Hkv, batch);
 #define DEC(DD, GG)                                                                                               \
   case GG:                                                                                                        \
-    launch_decode_dg<DD, GG>(grid, batch, Hkv, max_ctx, rows_per_split, nsplit, kc, vc, row_off, row_cap,        \
-                             cache_len, row_role, q, k_new, v_new, scale_log2, out, ws, status, stream);          \
+    launch_decode_dg<DD, GG>(grid, batch, Hkv, max_ctx, nsplit, kc, vc, row_off, row_cap, cache_len, row_role, q, \
+                             k_new, v_new, scale_log2, out, ws, status, stream);                                  \
     break;
 #define DEC_ALL_G(DD)                     \
   switch (G) {                            \

@@ -109,7 +109,7 @@ class CompactCache:
         key = (B, Hq, Hkv, d, int(max_ctx))
         if self.ws_key != key:
             n = sonic.decode_workspace_bytes(B, Hq, d, int(max_ctx))
-            self.ws = torch.empty(max(n, 256), dtype=torch.uint8, device=q.device)
+            self.ws = torch.zeros(max(n, 256), dtype=torch.uint8, device=q.device)   # counters start at zero
             self.ws_key = key
         return sonic.compressed_decode(self.k, self.v, self.row_off, self.row_cap, self.length, q, k_new, v_new,
                                        out, self.ws, status, max_ctx, row_role=row_role, stream=stream)
