@@ -189,6 +189,23 @@ def main():
     pf_ms, cp_ms, dc_ms = med(0, 1), med(1, 2), med(2, 3)
     step_ms_ev = med(0, 3)
 
+    # ---- back-to-back launches of the two single-launch phases (no graph-launch gap
+    # between phases): their per-launch rate ----
+    def back_to_back(f, n):
+        a, b_ = ev(), ev()
+        a.record(stream)
+        for _ in range(n):
+            if use_graph:
+                graphs[f].replay()
+            else:
+                phases[f]()
+        b_.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b_) / n
+    pf_b2b_ms = back_to_back("prefill", 10)
+    cp_b2b_ms = back_to_back("compact", 20)
+    assert db.read_status() == 0
+
     # ---- full-context decode (same kernel, text-only cache) for the speedup ----
     fms = []
     for _ in range(3):
@@ -248,6 +265,10 @@ def main():
             "prefill_frac_bf16_peak": round(prefill_tflops / PEAK_BF16_TFLOPS, 4),
             "compact_us": round(cp_ms * 1e3, 2), "compact_gbs": round(compact_gbs, 1),
             "compact_frac_hbm_peak": round(compact_gbs / PEAK_HBM_GBS, 4),
+            "prefill_ms_back_to_back": round(pf_b2b_ms, 4),
+            "prefill_visible_tflops_back_to_back": round(visible_flops / (pf_b2b_ms * 1e-3) / 1e12, 2),
+            "compact_us_back_to_back": round(cp_b2b_ms * 1e3, 2),
+            "compact_gbs_back_to_back": round(compact_bytes / (cp_b2b_ms * 1e-3) / 1e9, 1),
             "decode_ms_256_steps": round(dc_ms, 4), "decode_us_per_step": round(dc_ms * 1e3 / steps_dec, 2),
             "decode_tok_s": round(decode_tok_s, 1), "decode_gbs": round(decode_gbs, 1),
             "decode_frac_hbm_peak": round(decode_gbs / PEAK_HBM_GBS, 4),

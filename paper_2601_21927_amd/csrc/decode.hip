@@ -89,6 +89,10 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
   // row-fragment reads of the scores, V for the transposing reads); reused for the
   // merge of the waves at the end
   __shared__ __align__(16) uint16_t ring[kDecWaves * 2 * 2 * SLOT];
+  // each wave's copy of the G query rows (direct-to-LDS, so that no load the
+  // compiler counts precedes the pipeline's)
+  constexpr int NQ = (G * D * 2 + 1023) / 1024;   // direct-to-LDS instructions for Q
+  __shared__ __align__(16) uint16_t q_lds[kDecWaves][NQ * 512];
   __shared__ float m_lds[kDecWaves][16];
   __shared__ float l_lds[kDecWaves][16];
   __shared__ int s_last;
@@ -130,15 +134,24 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
     *reinterpret_cast<u32x4 *>(vbase + dst) = reinterpret_cast<const u32x4 *>(vnew)[threadIdx.x];
   }
 
-  // Q^T fragments (B operand of the scores): lane (col, quarter) holds d = 32*ks +
-  // 8*quarter .. +7 of q-head kvh*G + col (columns col >= G load head kvh*G and are
-  // never read back).
-  bf16x8 qf[KS];
+  // The wave's Q rows go to q_lds (lanes past the G rows fetch row 0 again); the
+  // Q^T fragments (B operand of the scores) are read from there once the first wait
+  // has passed: lane (col, quarter) takes d = 32*ks + 8*quarter .. +7 of q-head
+  // kvh*G + col (columns col >= G take head kvh*G and are never read back).
   {
-    const uint16_t *qrow = q + (static_cast<size_t>(b) * Hq + kvh * G + (col < G ? col : 0)) * D;
+    const uint16_t *q0 = q + (static_cast<size_t>(b) * Hq + kvh * G) * D;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const bf16x8 *>(qrow + 32 * ks + 8 * quarter);
+    for (int i = 0; i < NQ; ++i) {
+      const int e = (i * kWave + lane) * 8;   // element of the [G][D] block
+      dma16(q0 + (e < G * D ? e : e % D), &q_lds[wave][i * 512]);
+    }
   }
+  bf16x8 qf[KS];
+  auto read_q = [&]() {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qf[ks] = *reinterpret_cast<const bf16x8 *>(&q_lds[wave][(col < G ? col : 0) * D + 32 * ks + 8 * quarter]);
+  };
 
   // Row r of the context: the cache below len, the new token at len.  Rows past the
   // split's end load row r_begin instead (and are masked), so every group issues the
@@ -243,14 +256,18 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
   // two-deep pipeline: group j + 2 is issued as soon as group j has left its slot
   issue(0, 0);
   issue(1, 1);
-  for (int j = 0; j < iters; j += 2) {
+  wait_vm<NG>();                        // Q and group 0 have landed (group 1 may not have)
+  read_q();
+  process(0, 0);
+  issue(2, 0);
+  for (int j = 1; j < iters; j += 2) {
     wait_vm<NG>();                      // group j has landed (group j + 1 may not have)
-    process(j, 0);
-    issue(j + 2, 0);
+    process(j, 1);
+    issue(j + 2, 1);
     if (j + 1 >= iters) break;
     wait_vm<NG>();
-    process(j + 1, 1);
-    issue(j + 3, 1);
+    process(j + 1, 0);
+    issue(j + 3, 0);
   }
   wait_vm<0>();   // the trailing (unused) loads, before the ring is reused
 
