@@ -192,12 +192,18 @@ def main():
     # ---- back-to-back launches of the two single-launch phases (no graph-launch gap
     # between phases): their per-launch rate ----
     def back_to_back(f, n):
+        if use_graph:   # n calls in one graph, so no graph launch separates them
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for _ in range(n):
+                    phases[f]()
+            torch.cuda.synchronize()
         a, b_ = ev(), ev()
         a.record(stream)
-        for _ in range(n):
-            if use_graph:
-                graphs[f].replay()
-            else:
+        if use_graph:
+            g.replay()
+        else:
+            for _ in range(n):
                 phases[f]()
         b_.record(stream)
         torch.cuda.synchronize()
