@@ -21,9 +21,12 @@ those definitions out, slowly and in float64:
 * ``decode``     - generation over the retained context {I_sys, N, Q_n}
                    (App. C, Eq.(15)) and the same step over the full cache with
                    the mask applied.
+* ``extend``     - the next turn's Nexus rows over the compact cache (Sec. 3.2
+                   mask restricted to the newest segment) and the cache update
+                   that drops the turn's body and keeps its Nexus KV.
 
 Inputs are bf16 bit patterns (uint16); they are widened exactly to float64.
 """
-from . import layout, mask, attention, compaction, decode  # noqa: F401
+from . import layout, mask, attention, compaction, decode, extend  # noqa: F401
 
-__all__ = ["layout", "mask", "attention", "compaction", "decode"]
+__all__ = ["layout", "mask", "attention", "compaction", "decode", "extend"]

@@ -291,6 +291,27 @@ def random_layout(rng: np.random.Generator, max_h=4, max_b=80, max_k=40, max_s=7
     return RequestLayout(int(rng.integers(0, max_s + 1)), bodies, nexus, int(rng.integers(0, max_c + 1)))
 
 
+def extend_positions(lay: RequestLayout):
+    """Positions (in the layout) of a next-turn Nexus step for the layout's last segment:
+    (cache rows in order: system, earlier segments' Nexus, the last body; rows kept
+    afterwards; positions of the last segment's Nexus rows).  The layout must have at
+    least one segment and no current-query tokens."""
+    if not lay.bodies or lay.current:
+        raise ValueError("needs a history segment last and no current query")
+    p = lay.system
+    cache = list(range(lay.system))
+    for i, (b, k) in enumerate(zip(lay.bodies, lay.nexus)):
+        last = i == len(lay.bodies) - 1
+        if last:
+            cache += list(range(p, p + b))
+            nexus = list(range(p + b, p + b + k))
+        else:
+            cache += list(range(p + b, p + b + k))
+        p += b + k
+    keep = lay.system + sum(lay.nexus[:-1])
+    return np.array(cache, np.int64), keep, np.array(nexus, np.int64)
+
+
 def text_only_layout(lay: RequestLayout) -> RequestLayout:
     """The same conversation without Nexus tokens: what a full-context model keeps."""
     return RequestLayout(lay.system, list(lay.bodies), [0] * len(lay.bodies), lay.current)
