@@ -12,7 +12,11 @@
  *   sonic_kv_compact            - the KV retention rule (Sec. 3, Fig. 2 caption;
  *                                 Sec. 3.2 after Eq.(4); App. C);
  *   sonic_compressed_decode     - one generation step over the retained context
- *                                 {I_sys, N, Q_n} (App. C, Eq.(15)).
+ *                                 {I_sys, N, Q_n} (App. C, Eq.(15));
+ *   sonic_nexus_extend          - when a turn ends, its Nexus tokens over the
+ *                                 compact cache, then the turn's rows replaced
+ *                                 by their Nexus KV (Sec. 3.2; the Nexus KV is
+ *                                 kept for the rest of the session).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -216,6 +220,53 @@ int32_t sonic_compressed_decode(int32_t batch, int32_t num_q_heads, int32_t num_
                                 const void *q, const void *k_new, const void *v_new, float softmax_scale,
                                 float *out, void *workspace, size_t workspace_bytes, int32_t *dev_status,
                                 void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Next turn: the ended turn's Nexus tokens over the compact cache            */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of device workspace sonic_nexus_extend needs (0 for negative sizes). */
+size_t sonic_nexus_extend_workspace_bytes(int32_t batch, int32_t total_new);
+
+/*
+ * When turn n of request b ends, its rows (query and generated response) are the
+ * last rows of the request's compact cache, rows keep_len[b] .. cache_len[b]-1;
+ * they become the body of a new history segment, followed by that segment's
+ * Nexus tokens (Eq.(1)).  For every new Nexus row p and q-head h
+ *     out[p][h] = softmax_q(scale * <q[p][h], k[q][g(h)]>) v[q][g(h)]
+ * over q in {the request's cache rows 0 .. cache_len[b]-1} u {its new Nexus rows}:
+ * by Sec. 3.2 a Nexus row of the newest segment sees the system prompt and the
+ * earlier segments' Nexus tokens (Eq.(3)), its own body (Eq.(4)) and all the
+ * Nexus tokens of its segment (Eq.(5)), which are exactly these rows.  The
+ * result does not depend on whether Nexus tokens see later segments' Nexus
+ * tokens, since none exist yet.  Then the new Nexus K/V are written to cache
+ * rows keep_len[b] .. over the turn's body, which no later row may see (Eq.(4)),
+ * and cache_len[b] becomes keep_len[b] + (number of new Nexus rows of b).
+ *
+ *   batch, total_new   B and N = nexus_cu[B] (host values); a request may have
+ *                      no new Nexus rows (its body is then only dropped)
+ *   max_rows           host bound: cache_len[b] <= max_rows for every b
+ *   nexus_cu           device int32 [B+1], non-decreasing, nexus_cu[0] = 0:
+ *                      request b's new Nexus rows are rows nexus_cu[b] .. of q/k/v
+ *   keep_len           device int32 [B]: cache rows kept (system prompt and the
+ *                      earlier Nexus tokens), 0 <= keep_len[b] <= cache_len[b]
+ *   k_cache .. cache_len   the compact cache, as for sonic_compressed_decode
+ *   q                  device bf16 [N][Hq][d];  k, v: device bf16 [N][Hkv][d]
+ *   out                device fp32 [N][Hq][d]
+ *   workspace          device, 256-byte aligned, >= sonic_nexus_extend_workspace_bytes(B, N);
+ *                      contents need no initialisation
+ *   dev_status         SONIC_ERR_BAD_LAYOUT when nexus_cu or the lengths are
+ *                      inconsistent, SONIC_ERR_CAPACITY when keep_len[b] plus the new
+ *                      rows exceed the capacity; then (as with any pending status)
+ *                      nothing is written
+ * Returns SONIC_ERR_UNSUPPORTED when max_rows or N rows of one tensor reach 4 GiB.
+ */
+int32_t sonic_nexus_extend(int32_t batch, int32_t total_new, int32_t num_q_heads, int32_t num_kv_heads,
+                           int32_t head_dim, int32_t max_rows, const int32_t *nexus_cu, const int32_t *keep_len,
+                           void *k_cache, void *v_cache, const int64_t *cache_row_off,
+                           const int32_t *cache_row_cap, int32_t *cache_len, const void *q, const void *k,
+                           const void *v, float softmax_scale, float *out, void *workspace,
+                           size_t workspace_bytes, int32_t *dev_status, void *stream);
 
 #ifdef __cplusplus
 }

@@ -13,8 +13,15 @@ hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus,
                        const uint8_t *role, const int32_t *turn, const uint16_t *k, const uint16_t *v, PrefillWs ws,
                        int32_t *status, hipStream_t stream);
 hipError_t prefill_occupancy(int D, int G, int *blocks);
-hipError_t launch_prefill(int D, int G, int grid, const int32_t *cu, const uint16_t *q, const uint16_t *k,
-                          const uint16_t *v, float *out, PrefillWs ws, int Hkv, float scale_log2, hipStream_t stream);
+hipError_t launch_plan_extend(int batch, int total_new, int max_rows, const int32_t *nexus_cu,
+                              const int32_t *keep_len, const int32_t *cache_len, const int32_t *row_cap,
+                              PrefillWs ws, int32_t *status, hipStream_t stream);
+hipError_t launch_extend_append(int batch, int max_new, int Hkv, int D, const int32_t *nexus_cu,
+                                const int32_t *keep_len, uint16_t *kc, uint16_t *vc, const int64_t *row_off,
+                                int32_t *cache_len, const uint16_t *k_new, const uint16_t *v_new,
+                                const int32_t *status, hipStream_t stream);
+hipError_t launch_prefill(int D, int G, int grid, AttnRows rows, PrefillWs ws, int Hkv, float scale_log2,
+                          hipStream_t stream);
 hipError_t launch_compact(int batch, int total_tokens, int max_seqlen, int Hkv, int D, const int32_t *cu,
                           const uint8_t *role,
                           const uint16_t *k, const uint16_t *v, uint16_t *kc, uint16_t *vc, const int64_t *row_off,
@@ -28,7 +35,7 @@ hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int nsp
 
 namespace {
 
-constexpr int kAbiVersion = 2;
+constexpr int kAbiVersion = 3;
 constexpr double kLog2e = 1.4426950408889634;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -259,9 +266,90 @@ int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t 
   if (e != hipSuccess) return SONIC_ERR_HIP;
   int grid = di->num_cus * di->prefill_blocks[d == 128][G];
   grid = (grid + kNumXcd - 1) / kNumXcd * kNumXcd;
-  e = launch_prefill(d, G, grid, cu_seqlens, static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k),
-                     static_cast<const uint16_t *>(v), out, ws, Hkv, static_cast<float>(softmax_scale * kLog2e),
-                     stream);
+  AttnRows rows{cu_seqlens, nullptr, static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k),
+                static_cast<const uint16_t *>(v), ws.k_pre, ws.v_pre, out};
+  e = launch_prefill(d, G, grid, rows, ws, Hkv, static_cast<float>(softmax_scale * kLog2e), stream);
+  return finish(e, dev_status, stream);
+}
+
+// ---------------------------------------------------------------- next-turn Nexus step
+static size_t extend_ws_layout(int32_t batch, int32_t total_new, PrefillWs *ws, char *base) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes, 256);
+    return base ? base + o : nullptr;
+  };
+  const size_t B1 = static_cast<size_t>(batch > 0 ? batch : 1);
+  const size_t N1 = static_cast<size_t>(total_new > 0 ? total_new : 1);
+  char *req = take(sizeof(ReqInfo) * B1);
+  char *req_off = take(sizeof(int32_t) * B1);
+  char *tiles = take(sizeof(TileDesc) * N1);
+  char *order = take(sizeof(int32_t) * N1);
+  char *ctrl = take(sizeof(int32_t) * 16);
+  if (ws) {
+    *ws = PrefillWs{};
+    ws->req = reinterpret_cast<ReqInfo *>(req);
+    ws->req_off = reinterpret_cast<int32_t *>(req_off);
+    ws->tiles = reinterpret_cast<TileDesc *>(tiles);
+    ws->order = reinterpret_cast<int32_t *>(order);
+    ws->ctrl = reinterpret_cast<int32_t *>(ctrl);
+  }
+  return off;
+}
+
+size_t sonic_nexus_extend_workspace_bytes(int32_t batch, int32_t total_new) {
+  if (batch < 0 || total_new < 0) return 0;
+  return extend_ws_layout(batch, total_new, nullptr, nullptr);
+}
+
+int32_t sonic_nexus_extend(int32_t batch, int32_t total_new, int32_t Hq, int32_t Hkv, int32_t d, int32_t max_rows,
+                           const int32_t *nexus_cu, const int32_t *keep_len, void *k_cache, void *v_cache,
+                           const int64_t *cache_row_off, const int32_t *cache_row_cap, int32_t *cache_len,
+                           const void *q, const void *k, const void *v, float softmax_scale, float *out,
+                           void *workspace, size_t workspace_bytes, int32_t *dev_status, void *stream_) {
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  if (batch < 0 || total_new < 0 || Hq <= 0 || Hkv <= 0 || max_rows < 0 || dev_status == nullptr)
+    return SONIC_ERR_INVALID_ARG;
+  if (d != 64 && d != 128) return SONIC_ERR_UNSUPPORTED;
+  if (Hq % Hkv != 0) return SONIC_ERR_INVALID_ARG;
+  const int G = Hq / Hkv;
+  if (G > 8) return SONIC_ERR_UNSUPPORTED;
+  if (batch > 65535) return SONIC_ERR_UNSUPPORTED;
+  if (!std::isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SONIC_ERR_INVALID_ARG;
+  if (batch == 0) return SONIC_OK;
+  if (!nexus_cu || !keep_len || !k_cache || !v_cache || !cache_row_off || !cache_row_cap || !cache_len ||
+      !workspace || (total_new > 0 && (!q || !k || !v || !out)))
+    return SONIC_ERR_INVALID_ARG;
+  if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) ||
+      !aligned(out, 16) || !aligned(workspace, 256))
+    return SONIC_ERR_INVALID_ARG;
+  // cache and new rows are addressed with 32-bit byte offsets inside one request
+  const size_t row_bytes = static_cast<size_t>(Hkv) * d * 2;
+  if (static_cast<size_t>(max_rows) * row_bytes >= (size_t(1) << 32) ||
+      static_cast<size_t>(total_new) * row_bytes >= (size_t(1) << 32))
+    return SONIC_ERR_UNSUPPORTED;
+  PrefillWs ws;
+  const size_t need = extend_ws_layout(batch, total_new, &ws, static_cast<char *>(workspace));
+  if (workspace_bytes < need) return SONIC_ERR_WORKSPACE;
+  DeviceInfo *di = nullptr;
+  hipError_t e = device_info(&di);
+  if (e != hipSuccess) return SONIC_ERR_HIP;
+  e = launch_plan_extend(batch, total_new, max_rows, nexus_cu, keep_len, cache_len, cache_row_cap, ws, dev_status,
+                         stream);
+  if (e != hipSuccess) return SONIC_ERR_HIP;
+  if (total_new > 0) {
+    int grid = di->num_cus * di->prefill_blocks[d == 128][G];
+    grid = (grid + kNumXcd - 1) / kNumXcd * kNumXcd;
+    AttnRows rows{nexus_cu, cache_row_off, static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k),
+                  static_cast<const uint16_t *>(v), static_cast<const uint16_t *>(k_cache),
+                  static_cast<const uint16_t *>(v_cache), out};
+    e = launch_prefill(d, G, grid, rows, ws, Hkv, static_cast<float>(softmax_scale * kLog2e), stream);
+    if (e != hipSuccess) return SONIC_ERR_HIP;
+  }
+  e = launch_extend_append(batch, total_new, Hkv, d, nexus_cu, keep_len, static_cast<uint16_t *>(k_cache),
+                           static_cast<uint16_t *>(v_cache), cache_row_off, cache_len,
+                           static_cast<const uint16_t *>(k), static_cast<const uint16_t *>(v), dev_status, stream);
   return finish(e, dev_status, stream);
 }
 

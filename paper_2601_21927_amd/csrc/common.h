@@ -77,6 +77,21 @@ struct ReqInfo {
   int64_t pad;
 };
 
+// Where the rows of an attention call live.  Request b's query rows (and output
+// rows) start at row seg_row0[b] of q/out, its own key rows at row seg_row0[b] of
+// seg_k/seg_v, and its prefix rows at row pre_row0[b] of pre_k/pre_v (row
+// seg_row0[b] when pre_row0 is null).  Rows are [H, D] records.
+struct AttnRows {
+  const int32_t *seg_row0;
+  const int64_t *pre_row0;
+  const uint16_t *q;
+  const uint16_t *seg_k;
+  const uint16_t *seg_v;
+  const uint16_t *pre_k;
+  const uint16_t *pre_v;
+  float *out;
+};
+
 // Device workspace of the prefill, carved from one caller buffer.
 struct PrefillWs {
   ReqInfo *req;        // [B]

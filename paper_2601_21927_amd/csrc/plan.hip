@@ -280,12 +280,20 @@ __global__ __launch_bounds__(kGatherThreads) void gather_prefix_kernel(int batch
   }
 }
 
+// Work order of the descriptors of a batch (request b's at offset cu[b] of ws.tiles)
+// and reset queues; shared by the prefill and the next-turn Nexus step.
+hipError_t launch_plan_order(int batch, const int32_t *cu, PrefillWs ws, int32_t *status, hipStream_t stream) {
+  plan_rank_kernel<<<dim3(1), dim3(kPlanThreads), 0, stream>>>(batch, ws, status);
+  plan_order_kernel<<<dim3(batch), dim3(kPlanThreads), 0, stream>>>(cu, ws, status);
+  return hipGetLastError();
+}
+
 hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus, const int32_t *cu,
                        const uint8_t *role, const int32_t *turn, const uint16_t *k, const uint16_t *v, PrefillWs ws,
                        int32_t *status, hipStream_t stream) {
   plan_runs_kernel<<<dim3(batch), dim3(kPlanThreads), 0, stream>>>(cu, role, turn, ws, total_tokens, status);
-  plan_rank_kernel<<<dim3(1), dim3(kPlanThreads), 0, stream>>>(batch, ws, status);
-  plan_order_kernel<<<dim3(batch), dim3(kPlanThreads), 0, stream>>>(cu, ws, status);
+  hipError_t e = launch_plan_order(batch, cu, ws, status, stream);
+  if (e != hipSuccess) return e;
   const int row_pieces = Hkv * D / 8;
   const long long total = static_cast<long long>(total_tokens) * row_pieces;
   long long want = (total + kGatherThreads - 1) / kGatherThreads;

@@ -132,11 +132,10 @@ __device__ __forceinline__ void stage_tensor(uint16_t *lds_buf, const char *pre_
 }
 
 template <int D, int G>
-__global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__restrict__ cu,
-                                                               const uint16_t *__restrict__ q,
-                                                               const uint16_t *__restrict__ k,
-                                                               const uint16_t *__restrict__ v, float *__restrict__ out,
-                                                               PrefillWs ws, int Hkv, float scale_log2) {
+__global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, PrefillWs ws, int Hkv,
+                                                               float scale_log2) {
+  const uint16_t *__restrict__ q = rows.q;
+  float *__restrict__ out = rows.out;
   constexpr int DC = D / 8;              // 16-byte chunks per K/V row
   constexpr int DS = D / 16;             // d steps of the S product
   constexpr int DB = D / 32;             // 32-wide d blocks of the output
@@ -174,7 +173,8 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
     const int slot = ws.order[item / Hkv];
     const int kvh = item % Hkv;
     const TileDesc t = ws.tiles[slot];
-    const int base = cu[t.req];
+    const int base = rows.seg_row0[t.req];
+    const int64_t pbase = rows.pre_row0 != nullptr ? rows.pre_row0[t.req] : static_cast<int64_t>(base);
     const int h = kvh * G + wave;
     const int nv = tile_key_count(t);
     const int nF = nv - t.ndiag;
@@ -182,12 +182,13 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
     const int seg_shift = t.seg_start - npre;    // request position of virtual key vk >= npre
     const size_t tok_stride = static_cast<size_t>(Hkv) * D;
     const size_t head0 = static_cast<size_t>(base) * tok_stride + static_cast<size_t>(kvh) * D;
-    // row 0 of the request (and of its prefix copy) for this kv-head; rows are
+    const size_t phead0 = static_cast<size_t>(pbase) * tok_stride + static_cast<size_t>(kvh) * D;
+    // row 0 of the request (and of its prefix rows) for this kv-head; rows are
     // row_bytes apart, and every row of a request lies below 4 GiB from its row 0
-    const char *kreq = reinterpret_cast<const char *>(k + head0);
-    const char *vreq = reinterpret_cast<const char *>(v + head0);
-    const char *kpre = reinterpret_cast<const char *>(ws.k_pre + head0);
-    const char *vpre = reinterpret_cast<const char *>(ws.v_pre + head0);
+    const char *kreq = reinterpret_cast<const char *>(rows.seg_k + head0);
+    const char *vreq = reinterpret_cast<const char *>(rows.seg_v + head0);
+    const char *kpre = reinterpret_cast<const char *>(rows.pre_k + phead0);
+    const char *vpre = reinterpret_cast<const char *>(rows.pre_v + phead0);
     const uint32_t row_bytes = static_cast<uint32_t>(tok_stride * 2);
 
     auto stage_k = [&](int c, uint16_t *buf) {
@@ -346,10 +347,9 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(const int32_t *__
 }
 
 template <int D, int G>
-static hipError_t launch_prefill_dg(int grid, const int32_t *cu, const uint16_t *q, const uint16_t *k,
-                                    const uint16_t *v, float *out, PrefillWs ws, int Hkv, float scale_log2,
+static hipError_t launch_prefill_dg(int grid, AttnRows rows, PrefillWs ws, int Hkv, float scale_log2,
                                     hipStream_t stream) {
-  prefill_kernel<D, G><<<dim3(grid), dim3(G * kWave), 0, stream>>>(cu, q, k, v, out, ws, Hkv, scale_log2);
+  prefill_kernel<D, G><<<dim3(grid), dim3(G * kWave), 0, stream>>>(rows, ws, Hkv, scale_log2);
   return hipGetLastError();
 }
 
@@ -382,10 +382,9 @@ hipError_t prefill_occupancy(int D, int G, int *blocks) {
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_prefill(int D, int G, int grid, const int32_t *cu, const uint16_t *q, const uint16_t *k,
-                          const uint16_t *v, float *out, PrefillWs ws, int Hkv, float scale_log2,
+hipError_t launch_prefill(int D, int G, int grid, AttnRows rows, PrefillWs ws, int Hkv, float scale_log2,
                           hipStream_t stream) {
-#define LAUNCH(DD, GG) return launch_prefill_dg<DD, GG>(grid, cu, q, k, v, out, ws, Hkv, scale_log2, stream)
+#define LAUNCH(DD, GG) return launch_prefill_dg<DD, GG>(grid, rows, ws, Hkv, scale_log2, stream)
   if (D == 64) {
     SONIC_FOR_G(64, LAUNCH)
   } else if (D == 128) {

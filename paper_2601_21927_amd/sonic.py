@@ -30,7 +30,8 @@ ROLE_SYSTEM, ROLE_HISTORY_TEXT, ROLE_NEXUS, ROLE_CURRENT = 0, 1, 2, 3
 EXPORTS = (
     "sonic_abi_version", "sonic_status_string", "sonic_validate_layout_host", "sonic_layout_stats_host",
     "sonic_prefill_workspace_bytes", "sonic_segment_attn_prefill", "sonic_kv_compact",
-    "sonic_decode_workspace_bytes", "sonic_compressed_decode",
+    "sonic_decode_workspace_bytes", "sonic_compressed_decode", "sonic_nexus_extend_workspace_bytes",
+    "sonic_nexus_extend",
 )
 
 _lib = None
@@ -72,6 +73,11 @@ def lib() -> ctypes.CDLL:
     L.sonic_compressed_decode.restype = _i32
     L.sonic_compressed_decode.argtypes = [_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _f32,
                                           _p, _p, _sz, _p, _p]
+    L.sonic_nexus_extend_workspace_bytes.restype = _sz
+    L.sonic_nexus_extend_workspace_bytes.argtypes = [_i32, _i32]
+    L.sonic_nexus_extend.restype = _i32
+    L.sonic_nexus_extend.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p,
+                                     _f32, _p, _p, _sz, _p, _p]
     _lib = L
     return L
 
@@ -105,6 +111,16 @@ def _dev(*ts):
     for t in ts:
         if t is not None and not t.is_cuda:
             raise ValueError("libsonic GPU entry points take device tensors")
+
+
+_I32, _I64, _U8, _BF16, _F32 = torch.int32, torch.int64, torch.uint8, torch.bfloat16, torch.float32
+
+
+def _types(**named):
+    """named=(tensor, dtype): the C ABI reads raw memory, so a wrong element type is refused here."""
+    for name, (t, dt) in named.items():
+        if t is not None and t.dtype != dt:
+            raise TypeError(f"{name} must be {dt}, got {t.dtype}")
 
 
 # ----------------------------------------------------------------- host helpers
@@ -144,6 +160,8 @@ def segment_attn_prefill(cu_seqlens, role, turn_id, q, k, v, out, workspace, dev
     """q [T,Hq,d] bf16, k/v [T,Hkv,d] bf16, out [T,Hq,d] fp32; cu int32 [B+1]; role uint8 [T];
     turn_id int32 [T]; workspace uint8 [>= prefill_workspace_bytes]; dev_status int32 [1]."""
     _dev(cu_seqlens, role, turn_id, q, k, v, out, workspace, dev_status)
+    _types(cu_seqlens=(cu_seqlens, _I32), role=(role, _U8), turn_id=(turn_id, _I32), q=(q, _BF16), k=(k, _BF16),
+           v=(v, _BF16), out=(out, _F32), dev_status=(dev_status, _I32))
     T, Hq, d = q.shape
     Hkv = k.shape[1]
     scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
@@ -159,6 +177,9 @@ def kv_compact(cu_seqlens, role, k, v, k_cache, v_cache, cache_row_off, cache_ro
     """k/v [T,Hkv,d] bf16 -> k_cache/v_cache [rows,Hkv,d]; cache_row_off int64 [B]; cache_row_cap int32 [B];
     cache_len int32 [B]; keep_idx int32 [rows]."""
     _dev(cu_seqlens, role, k, v, k_cache, v_cache, cache_row_off, cache_row_cap, cache_len, keep_idx, dev_status)
+    _types(cu_seqlens=(cu_seqlens, _I32), role=(role, _U8), k=(k, _BF16), v=(v, _BF16), k_cache=(k_cache, _BF16),
+           v_cache=(v_cache, _BF16), cache_row_off=(cache_row_off, _I64), cache_row_cap=(cache_row_cap, _I32),
+           cache_len=(cache_len, _I32), keep_idx=(keep_idx, _I32), dev_status=(dev_status, _I32))
     T, Hkv, d = k.shape
     return int(lib().sonic_kv_compact(
         cu_seqlens.numel() - 1, T, int(max_seqlen), Hkv, d, _ptr(cu_seqlens), _ptr(role), _ptr(k), _ptr(v),
@@ -176,6 +197,9 @@ def compressed_decode(k_cache, v_cache, cache_row_off, cache_row_cap, cache_len,
     """q [B,Hq,d] bf16; k_new/v_new [B,Hkv,d] bf16; out [B,Hq,d] fp32; row_role uint8 [rows] or None."""
     _dev(k_cache, v_cache, cache_row_off, cache_row_cap, cache_len, q, k_new, v_new, out, workspace, dev_status,
          row_role)
+    _types(k_cache=(k_cache, _BF16), v_cache=(v_cache, _BF16), cache_row_off=(cache_row_off, _I64),
+           cache_row_cap=(cache_row_cap, _I32), cache_len=(cache_len, _I32), q=(q, _BF16), k_new=(k_new, _BF16),
+           v_new=(v_new, _BF16), out=(out, _F32), dev_status=(dev_status, _I32), row_role=(row_role, _U8))
     B, Hq, d = q.shape
     Hkv = k_new.shape[1]
     scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
@@ -183,3 +207,26 @@ def compressed_decode(k_cache, v_cache, cache_row_off, cache_row_cap, cache_len,
         B, Hq, Hkv, d, int(max_ctx), _ptr(k_cache), _ptr(v_cache), _ptr(cache_row_off), _ptr(cache_row_cap),
         _ptr(cache_len), _ptr(row_role), _ptr(q), _ptr(k_new), _ptr(v_new), scale, _ptr(out), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _ptr(dev_status), _stream(stream)))
+
+
+# ----------------------------------------------------------------- next turn: Nexus step
+def nexus_extend_workspace_bytes(batch: int, total_new: int) -> int:
+    return int(lib().sonic_nexus_extend_workspace_bytes(batch, total_new))
+
+
+def nexus_extend(nexus_cu, keep_len, k_cache, v_cache, cache_row_off, cache_row_cap, cache_len, q, k, v, out,
+                 workspace, dev_status, max_rows: int, softmax_scale=None, stream=None) -> int:
+    """nexus_cu int32 [B+1]; keep_len int32 [B]; q [N,Hq,d] bf16; k/v [N,Hkv,d] bf16; out [N,Hq,d] fp32."""
+    _dev(nexus_cu, keep_len, k_cache, v_cache, cache_row_off, cache_row_cap, cache_len, q, k, v, out, workspace,
+         dev_status)
+    _types(nexus_cu=(nexus_cu, _I32), keep_len=(keep_len, _I32), k_cache=(k_cache, _BF16), v_cache=(v_cache, _BF16),
+           cache_row_off=(cache_row_off, _I64), cache_row_cap=(cache_row_cap, _I32), cache_len=(cache_len, _I32),
+           q=(q, _BF16), k=(k, _BF16), v=(v, _BF16), out=(out, _F32), dev_status=(dev_status, _I32))
+    N, Hq, d = q.shape
+    Hkv = k.shape[1]
+    scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    return int(lib().sonic_nexus_extend(
+        nexus_cu.numel() - 1, N, Hq, Hkv, d, int(max_rows), _ptr(nexus_cu), _ptr(keep_len), _ptr(k_cache),
+        _ptr(v_cache), _ptr(cache_row_off), _ptr(cache_row_cap), _ptr(cache_len), _ptr(q), _ptr(k), _ptr(v), scale,
+        _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(dev_status),
+        _stream(stream)))
