@@ -12,6 +12,9 @@ Prints one JSON line.  value = generated tokens per second of the whole step
 (B x 256 decode tokens / step time, the step including its prefill and
 compaction).  Per-phase figures, the roofline of the dominant kernel and the
 fp64 CPU oracle's rate on a bounded sample of the same work are attached.
+After the timed region, the next-turn Nexus step (the finished turn becomes a
+history segment whose Nexus rows attend to the whole cache) is timed on its
+own; it is reported as a phase and is not part of value.
 """
 from __future__ import annotations
 
@@ -228,6 +231,57 @@ def main():
     full_ms = float(np.median(fms))
     assert db.read_status() == 0
 
+    # ---- next-turn Nexus step: the turn that just ended (C query rows + the decoded rows)
+    # becomes segment h+1; its K Nexus rows attend to the whole cache, then replace the
+    # turn's rows.  The decode loop left those rows at kept..kept+steps of every request.
+    cu = batch.cu_seqlens
+    ext_keep_np = np.array([l.system + sum(l.nexus) for l in batch.layouts], np.int32)
+    ext_len_np = (kept + steps_dec).astype(np.int32)
+    npos = []   # the last segment's Nexus rows serve as the new segment's inputs
+    for b, l in enumerate(batch.layouts):
+        p0 = int(cu[b]) + l.system + sum(l.bodies) + sum(l.nexus[:-1])
+        npos.append(np.arange(p0, p0 + l.nexus[-1]))
+    kn_np = np.array([len(x) for x in npos], np.int64)
+    allpos = np.concatenate(npos)
+    ext_cu = torch.from_numpy(np.concatenate([[0], np.cumsum(kn_np)]).astype(np.int32)).to(dev)
+    ext_keep = torch.from_numpy(ext_keep_np).to(dev)
+    ext_len0 = torch.from_numpy(ext_len_np).to(dev)
+    ext_len = ext_len0.clone()
+    ext_k, ext_v = cache.k.clone(), cache.v.clone()
+    eq, ek, e_v = (bf16_to_device(x[allpos], dev) for x in (batch.q, batch.k, batch.v))
+    ext_out = torch.empty((len(allpos), Hq, d), dtype=torch.float32, device=dev)
+    ext_ws = torch.empty(max(sonic.nexus_extend_workspace_bytes(B, len(allpos)), 256), dtype=torch.uint8,
+                         device=dev)
+
+    def run_extend():
+        st = sonic.nexus_extend(ext_cu, ext_keep, ext_k, ext_v, cache.row_off, cache.row_cap, ext_len, eq, ek, e_v,
+                                ext_out, ext_ws, db.status, max_rows=max_ctx)
+        assert st == sonic.OK, sonic.status_string(st)
+
+    run_extend()
+    torch.cuda.synchronize()
+    if use_graph:
+        ext_graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(ext_graph):
+            run_extend()
+        torch.cuda.synchronize()
+    xms = []
+    for _ in range(20):
+        ext_len.copy_(ext_len0)     # the step consumes the turn's rows: start again from them
+        a, b_ = ev(), ev()
+        a.record(stream)
+        if use_graph:
+            ext_graph.replay()
+        else:
+            run_extend()
+        b_.record(stream)
+        torch.cuda.synchronize()
+        xms.append(a.elapsed_time(b_))
+    ext_ms = float(np.median(xms))
+    assert db.read_status() == 0, sonic.status_string(db.read_status())
+    assert np.array_equal(ext_len.cpu().numpy(), ext_keep_np + kn_np)
+    ext_flops = float(4 * d * Hq * np.sum(kn_np * (ext_len_np + kn_np)))
+
     # ---- algorithmic work ----
     row_bytes = Hkv * d * 2                       # one token's K (or V) over all kv-heads, bf16
     compact_bytes = float(kept.sum()) * row_bytes * 2 * 2 + batch.total_tokens + float(kept.sum()) * 4
@@ -281,9 +335,13 @@ def main():
             "full_context_decode_ms": round(full_ms, 4), "full_context_decode_gbs": round(full_bytes / (full_ms * 1e-3) / 1e9, 1),
             "decode_speedup_vs_full_context": round(full_ms / dc_ms, 3),
             "step_ms_event_median": round(step_ms_ev, 4),
+            "next_turn_nexus_us": round(ext_ms * 1e3, 2),
+            "next_turn_nexus_tflops": round(ext_flops / (ext_ms * 1e-3) / 1e12, 2),
+            "next_turn_nexus_frac_bf16_peak": round(ext_flops / (ext_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         },
         "work": {"visible_flops": visible_flops, "compact_bytes": compact_bytes, "decode_bytes": decode_bytes,
-                 "full_decode_bytes": full_bytes},
+                 "full_decode_bytes": full_bytes, "next_turn_nexus_flops": ext_flops,
+                 "next_turn_nexus": f"{len(allpos)} new Nexus rows over caches of {int(ext_len_np.max())} rows"},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
@@ -292,8 +350,8 @@ def main():
 
 
 def cpu_baseline(batch, kept):
-    """The fp64 oracle, as it stands, on a bounded sample of one step; scaled to tok/s."""
-    import threading  # noqa: F401
+    """The fp64 oracle, as it stands, on a bounded sample of one step (about 10 s of CPU
+    work); scaled to tok/s."""
     from oracle import attention as OA
     from oracle import compaction as OC
     from oracle import decode as OD
@@ -301,32 +359,43 @@ def cpu_baseline(batch, kept):
     cu = batch.cu_seqlens
     B = batch.batch
     steps = batch.decode_steps
-    # prefill: 96 query rows of request 0, scaled to all rows of the batch
-    s, e = int(cu[0]), int(cu[1])
-    rows = np.linspace(0, e - s - 1, 96).astype(np.int64)
+    rows_per_req, dec_per_req = 400, 64
+    # prefill: rows_per_req query rows of every request, spread over its length
     t0 = time.perf_counter()
-    OA.prefill_request(batch.q[s:e], batch.k[s:e], batch.v[s:e], batch.role[s:e], batch.turn_id[s:e], rows=rows)
-    t_pre = (time.perf_counter() - t0) * batch.total_tokens / len(rows)
-    # compaction: request 0, scaled to the batch
+    n_rows = 0
+    for b in range(B):
+        s, e = int(cu[b]), int(cu[b + 1])
+        rows = np.linspace(0, e - s - 1, rows_per_req).astype(np.int64)
+        OA.prefill_request(batch.q[s:e], batch.k[s:e], batch.v[s:e], batch.role[s:e], batch.turn_id[s:e],
+                           rows=rows)
+        n_rows += len(rows)
+    t_pre = (time.perf_counter() - t0) * batch.total_tokens / n_rows
+    # compaction: every request
     caps = kept.astype(np.int64)
-    kc = np.zeros((int(caps[0]), batch.num_kv_heads, batch.head_dim), np.uint16)
+    off = np.concatenate([[0], np.cumsum(caps)[:-1]]).astype(np.int64)
+    kc = np.zeros((int(caps.sum()), batch.num_kv_heads, batch.head_dim), np.uint16)
+    vc = kc.copy()
     t0 = time.perf_counter()
-    OC.compact_batch(batch.k[s:e], batch.v[s:e], batch.role[s:e], np.array([0, e - s]), [0], [caps[0]], kc,
-                     kc.copy(), np.zeros(int(caps[0]), np.int32))
-    t_cmp = (time.perf_counter() - t0) * B
-    # decode: 4 steps of request 0 (at the mean context of the loop), scaled to B x steps
-    t0 = time.perf_counter()
+    OC.compact_batch(batch.k, batch.v, batch.role, cu, off, caps, kc, vc, np.zeros(int(caps.sum()), np.int32))
+    t_cmp = time.perf_counter() - t0
+    # decode: dec_per_req steps of every request, from the middle of the loop, over its compact cache
+    # plus the decoded rows before them; scaled to B x steps
     mid = steps // 2
-    kctx = np.concatenate([kc, batch.dec_k[:mid, 0]])
-    for t in range(4):
-        OD.decode_step(batch.dec_q[mid + t, 0], kctx, kctx, batch.dec_k[mid + t, 0], batch.dec_v[mid + t, 0])
-    t_dec = (time.perf_counter() - t0) / 4 * B * steps
+    t0 = time.perf_counter()
+    for b in range(B):
+        o, n = int(off[b]), int(caps[b])
+        kctx = np.concatenate([kc[o:o + n], batch.dec_k[:mid, b]])
+        vctx = np.concatenate([vc[o:o + n], batch.dec_v[:mid, b]])
+        for t in range(dec_per_req):
+            OD.decode_step(batch.dec_q[mid + t, b], kctx, vctx, batch.dec_k[mid + t, b], batch.dec_v[mid + t, b])
+    t_dec = (time.perf_counter() - t0) / (B * dec_per_req) * B * steps
     total = t_pre + t_cmp + t_dec
     return {"value": round(B * steps / total, 3), "unit": "tok/s", "cores": cores, "kind": "oracle",
-            "sample": f"fp64 oracle: 96 prefill rows of request 0 (scaled to {batch.total_tokens} rows), "
-                      f"compaction of request 0 (scaled x{B}), 4 decode steps of request 0 at mid context "
-                      f"(scaled to {B}x{steps}); estimated step time {total:.1f} s",
+            "sample": f"fp64 oracle: {rows_per_req} prefill rows of each of the {B} requests (scaled to "
+                      f"{batch.total_tokens} rows), compaction of the whole batch, {dec_per_req} decode steps of each "
+                      f"request from mid-loop context (scaled to {B}x{steps}); estimated step time {total:.1f} s",
             "prefill_s_est": round(t_pre, 2), "compact_s_est": round(t_cmp, 3), "decode_s_est": round(t_dec, 2)}
+
 
 
 if __name__ == "__main__":
