@@ -23,8 +23,10 @@
 // hand-off does not go through them: the partials are stored write-through at
 // system scope and read back with loads that bypass the caches, which needs no
 // L2 writeback or invalidate (either would evict the K/V other workgroups are
-// streaming).  Finally the last pair of a request to finish advances cache_len:
-// by then every workgroup of the request has read the old length.
+// streaming).  Every split of a pair counts itself once per call, splits
+// without rows included, so the last to count knows that every workgroup of
+// the pair has read cache_len; it counts the pair for its request while it
+// loads the partials, and the last pair of a request advances cache_len.
 #include "common.h"
 
 namespace sonic {
@@ -35,7 +37,7 @@ constexpr int kGroupRows = 16;
 
 // Device workspace of the decode; the counters are zero between calls.
 struct DecodeWs {
-  int32_t *done;      // [B]      kv-heads of request b finished in this call
+  int32_t *done;      // [B]      kv-heads of request b whose splits have all counted in this call
   int32_t *arrive;    // [B*Hkv]  splits of a (request, kv-head) finished in this call
   float *part;        // [B*Hkv][nsplit][G*(D+2)] partial (m[G], l[G], acc[G][D]) per split
 };
@@ -61,6 +63,13 @@ __device__ __forceinline__ float load_sys(const float *p) {
   float v;
   asm volatile("global_load_dword %0, %1, off sc0 sc1" : "=v"(v) : "v"(p) : "memory");
   return v;
+}
+// atomic add of 1 returning the old value; the result register is written when the
+// atomic returns, so it is read only after an explicit wait_vm<0>
+__device__ __forceinline__ int atomic_inc_pending(int32_t *p) {
+  int old;
+  asm volatile("global_atomic_add %0, %1, %2, off sc0" : "=v"(old) : "v"(p), "v"(1) : "memory");
+  return old;
 }
 // s_waitcnt vmcnt(N), other counters at their maximum (gfx9 encoding)
 template <int N> __device__ __forceinline__ void wait_vm() {
@@ -93,6 +102,9 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
   // compiler counts precedes the pipeline's)
   constexpr int NQ = (G * D * 2 + 1023) / 1024;   // direct-to-LDS instructions for Q
   __shared__ __align__(16) uint16_t q_lds[kDecWaves][NQ * 512];
+  // split 0: the new token's k and v rows, fetched at the start and appended at the end
+  __shared__ __align__(16) uint16_t app_lds[kWave * 8];
+  static_assert(2 * DC <= kWave, "one direct-to-LDS instruction holds the new k and v rows");
   __shared__ float m_lds[kDecWaves][16];
   __shared__ float l_lds[kDecWaves][16];
   __shared__ int s_last;
@@ -112,11 +124,70 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
   // split ranges: R rows each, a multiple of the group size
   const int R = ((n_ctx + nsplit_max - 1) / nsplit_max + kGroupRows - 1) / kGroupRows * kGroupRows;
   const int nsp = (n_ctx + R - 1) / R;   // splits that hold rows; the others have nothing to do
-  if (split >= nsp) return;
+  const int nsplit = gridDim.x;
+  const int pair = b * Hkv + kvh;
+  float *orow = out + (static_cast<size_t>(b) * Hq + kvh * G) * D;
+
+  // Every split counts itself once, after its partial (if any) is stored.  The last
+  // to count merges the partials of the nsp splits with rows by log-sum-exp, a batch
+  // of eight per memory round trip, writes the output, and counts the pair for its
+  // request while the partials load; the last pair of a request advances the length.
+  auto finish_pair = [&]() {
+    if (threadIdx.x == 0) s_last = (atomicAdd(&ws.arrive[pair], 1) == nsplit - 1);
+    __syncthreads();
+    if (!s_last) return;
+    int old_done = 0;
+    if (threadIdx.x == 0) old_done = atomic_inc_pending(&ws.done[b]);
+    const float *recs = ws.part + static_cast<size_t>(pair) * nsplit_max * REC;
+    for (int idx = threadIdx.x; idx < G * D; idx += kDecThreads) {
+      const int hh = idx / D, dd = idx % D;
+      float M = -INFINITY, L = 0.f, A = 0.f;
+      for (int sp0 = 0; sp0 < nsp; sp0 += 8) {
+        float m[8], l[8], a[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const float *r = recs + static_cast<size_t>(min(sp0 + u, nsp - 1)) * REC + hh * (D + 2);
+          m[u] = load_sys(r);
+          l[u] = load_sys(r + 1);
+          a[u] = load_sys(r + 2 + dd);
+        }
+        wait_vm<0>();
+#pragma unroll
+        for (int u = 0; u < 8; ++u) asm volatile("" : "+v"(m[u]), "+v"(l[u]), "+v"(a[u]));
+        float Mb = M;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (sp0 + u < nsp) Mb = fmaxf(Mb, m[u]);
+        const float c = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mb);
+        L *= c;
+        A *= c;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const float w = (sp0 + u < nsp && m[u] != -INFINITY) ? __builtin_amdgcn_exp2f(m[u] - Mb) : 0.f;
+          L = fmaf(w, l[u], L);
+          A = fmaf(w, a[u], A);
+        }
+        M = Mb;
+      }
+      orow[idx] = A / L;
+    }
+    wait_vm<0>();
+    if (threadIdx.x == 0) {
+      asm volatile("" : "+v"(old_done));
+      ws.arrive[pair] = 0;
+      if (old_done == Hkv - 1) {
+        cache_len[b] = n_ctx;
+        ws.done[b] = 0;
+      }
+    }
+  };
+  if (split >= nsp) {   // no rows (only when nsplit > 1)
+    finish_pair();
+    return;
+  }
   const int r_begin = split * R;
   const int r_end = min(n_ctx, r_begin + R);
   const int ngroups = (r_end - r_begin + kGroupRows - 1) / kGroupRows;
-  const int iters = (ngroups + kDecWaves - 1) / kDecWaves;   // the same for every wave
   const int64_t base = row_off[b];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = threadIdx.x % kWave;
@@ -128,10 +199,14 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
   uint16_t *kbase = kc + static_cast<size_t>(base) * row_stride + static_cast<size_t>(kvh) * D;
   uint16_t *vbase = vc + static_cast<size_t>(base) * row_stride + static_cast<size_t>(kvh) * D;
 
-  if (split == 0 && threadIdx.x < DC) {   // append the new token at row len
-    const size_t dst = static_cast<size_t>(len) * row_stride + threadIdx.x * 8;
-    *reinterpret_cast<u32x4 *>(kbase + dst) = reinterpret_cast<const u32x4 *>(knew)[threadIdx.x];
-    *reinterpret_cast<u32x4 *>(vbase + dst) = reinterpret_cast<const u32x4 *>(vnew)[threadIdx.x];
+  // Split 0 appends the new token at row len.  Its rows go to LDS ahead of every other
+  // load of wave 0 (so the first wait covers them, and no wave waits for a load of its
+  // own before the pipeline starts); the stores happen after the streaming.  Rows of
+  // this call read the new token from k_new / v_new, so nothing here depends on them.
+  const bool appender = split == 0 && wave == 0;
+  if (appender) {
+    const int c = lane < 2 * DC ? lane % DC : 0;
+    dma16((lane >= DC && lane < 2 * DC ? vnew : knew) + c * 8, app_lds);
   }
 
   // The wave's Q rows go to q_lds (lanes past the G rows fetch row 0 again); the
@@ -161,12 +236,13 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
   auto vptr = [&](int r) { return r < len ? vbase + static_cast<size_t>(r) * row_stride : vnew; };
   uint16_t *my_ring = ring + wave * 4 * SLOT;
 
-  // group j of this wave covers rows r_begin + 16 * (wave + j * kDecWaves) ...
-  auto group_row0 = [&](int j) { return r_begin + kGroupRows * (wave + j * kDecWaves); };
-  // issue the loads of group j into ring slot s: lane -> (row, 16-byte position) of
+  // Group g of the split covers rows r_begin + 16 g ...; wave w takes groups w, w + 8,
+  // w + 16, ... (a fixed order, so the result does not depend on timing).
+  auto group_row0 = [&](int g) { return r_begin + kGroupRows * g; };
+  // issue the loads of group g into ring slot s: lane -> (row, 16-byte position) of
   // each instruction's rows; the position holds the row's swizzled chunk
-  auto issue = [&](int j, int s) {
-    const int r0 = group_row0(j);
+  auto issue = [&](int g, int s) {
+    const int r0 = group_row0(g);
     uint16_t *kslot = my_ring + s * 2 * SLOT;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
@@ -204,8 +280,8 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
   const int tr_off = tr_row * D + 4 * (col & 3);
   const int tr_swz = tr_row & VSWZ;
 
-  auto process = [&](int j, int s) {
-    const int r0 = group_row0(j);
+  auto process = [&](int g, int s) {
+    const int r0 = group_row0(g);
     const uint16_t *kslot = my_ring + s * 2 * SLOT;
     const uint32_t roles = MASKED ? load_roles(r0) : 0u;
     f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
@@ -253,23 +329,28 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
     __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));   // lgkmcnt(0): slot s may be refilled
   };
 
-  // two-deep pipeline: group j + 2 is issued as soon as group j has left its slot
-  issue(0, 0);
-  issue(1, 1);
-  wait_vm<NG>();                        // Q and group 0 have landed (group 1 may not have)
+  // two-deep pipeline: a slot is refilled as soon as its group has been processed
+  int ga = wave, gb = wave + kDecWaves;   // the groups in ring slots 0 and 1
+  issue(ga, 0);
+  issue(gb, 1);
+  wait_vm<NG>();                          // Q and slot 0 have landed (slot 1 may not have)
   read_q();
-  process(0, 0);
-  issue(2, 0);
-  for (int j = 1; j < iters; j += 2) {
-    wait_vm<NG>();                      // group j has landed (group j + 1 may not have)
-    process(j, 1);
-    issue(j + 2, 1);
-    if (j + 1 >= iters) break;
+  while (ga < ngroups) {
+    process(ga, 0);
+    ga += 2 * kDecWaves;
+    issue(ga, 0);
+    wait_vm<NG>();                        // slot 1 has landed (slot 0 may not have)
+    if (gb >= ngroups) break;
+    process(gb, 1);
+    gb += 2 * kDecWaves;
+    issue(gb, 1);
     wait_vm<NG>();
-    process(j + 1, 0);
-    issue(j + 3, 0);
   }
   wait_vm<0>();   // the trailing (unused) loads, before the ring is reused
+  if (appender && lane < 2 * DC) {
+    const size_t dst = static_cast<size_t>(len) * row_stride + (lane % DC) * 8;
+    *reinterpret_cast<u32x4 *>((lane < DC ? kbase : vbase) + dst) = *reinterpret_cast<const u32x4 *>(&app_lds[lane * 8]);
+  }
 
   // ---- merge: columns across the four quarters, then the waves through LDS ----
   l_run += __shfl_xor(l_run, 16);
@@ -288,8 +369,6 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
   }
   __syncthreads();
 
-  const int pair = b * Hkv + kvh;
-  float *orow = out + (static_cast<size_t>(b) * Hq + kvh * G) * D;
   float *rec = ws.part + (static_cast<size_t>(pair) * nsplit_max + split) * REC;
   for (int idx = threadIdx.x; idx < G * D; idx += kDecThreads) {
     const int hh = idx / D, dd = idx % D;
@@ -303,7 +382,7 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
       L = fmaf(sc, l_lds[w][hh], L);
       A = fmaf(sc, acc_lds[(w * G + hh) * D + dd], A);
     }
-    if (nsp == 1) {
+    if (nsplit == 1) {
       orow[idx] = A / L;
     } else {   // write-through at system scope (see the top of the file)
       if (dd == 0) {
@@ -313,54 +392,11 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
       __hip_atomic_store(rec + hh * (D + 2) + 2 + dd, A, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     }
   }
-  if (nsp > 1) {
+  if (nsplit > 1) {
     wait_vm<0>();      // this thread's partial is stored
     __syncthreads();   // ... and every thread's
-    if (threadIdx.x == 0) s_last = (atomicAdd(&ws.arrive[pair], 1) == nsp - 1);
-    __syncthreads();
-    if (!s_last) return;
-    // the last split merges every split's partial, a batch of eight per memory round trip
-    const float *recs = ws.part + static_cast<size_t>(pair) * nsplit_max * REC;
-    for (int idx = threadIdx.x; idx < G * D; idx += kDecThreads) {
-      const int hh = idx / D, dd = idx % D;
-      float M = -INFINITY, L = 0.f, A = 0.f;
-      for (int sp0 = 0; sp0 < nsp; sp0 += 8) {
-        float m[8], l[8], a[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const float *r = recs + static_cast<size_t>(min(sp0 + u, nsp - 1)) * REC + hh * (D + 2);
-          m[u] = load_sys(r);
-          l[u] = load_sys(r + 1);
-          a[u] = load_sys(r + 2 + dd);
-        }
-        wait_vm<0>();
-#pragma unroll
-        for (int u = 0; u < 8; ++u) asm volatile("" : "+v"(m[u]), "+v"(l[u]), "+v"(a[u]));
-        float Mb = M;
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-          if (sp0 + u < nsp) Mb = fmaxf(Mb, m[u]);
-        const float c = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mb);
-        L *= c;
-        A *= c;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const float w = (sp0 + u < nsp && m[u] != -INFINITY) ? __builtin_amdgcn_exp2f(m[u] - Mb) : 0.f;
-          L = fmaf(w, l[u], L);
-          A = fmaf(w, a[u], A);
-        }
-        M = Mb;
-      }
-      orow[idx] = A / L;
-    }
-    if (threadIdx.x == 0) ws.arrive[pair] = 0;
-  }
-  // the last kv-head of the request to finish advances the length: by then every
-  // workgroup of the request has read it
-  __syncthreads();
-  if (threadIdx.x == 0) s_last = (atomicAdd(&ws.done[b], 1) == Hkv - 1);
-  __syncthreads();
-  if (s_last && threadIdx.x == 0) {
+    finish_pair();
+  } else if (threadIdx.x == 0 && atomicAdd(&ws.done[b], 1) == Hkv - 1) {
     cache_len[b] = n_ctx;
     ws.done[b] = 0;
   }
