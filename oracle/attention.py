@@ -18,7 +18,7 @@ from __future__ import annotations
 import numpy as np
 
 from .layout import Parsed, parse
-from .mask import visibility_rows
+from .mask import NEXUS_ALL, visibility_rows
 
 
 def bf16_bits_to_f64(bits) -> np.ndarray:
@@ -40,7 +40,7 @@ def softmax_probs(scores: np.ndarray, vis: np.ndarray) -> np.ndarray:
     return e / e.sum(axis=1, keepdims=True)
 
 
-def request_probs(q, k, role, turn_id, h: int, scale=None, rows=None) -> np.ndarray:
+def request_probs(q, k, role, turn_id, h: int, scale=None, rows=None, nexus_scope: str = NEXUS_ALL) -> np.ndarray:
     """Attention probabilities P[rows, :] of q-head h of one request (float64)."""
     qf = bf16_bits_to_f64(q)
     kf = bf16_bits_to_f64(k)
@@ -49,14 +49,14 @@ def request_probs(q, k, role, turn_id, h: int, scale=None, rows=None) -> np.ndar
         scale = 1.0 / np.sqrt(d)
     L = qf.shape[0]
     r = np.arange(L) if rows is None else np.asarray(rows)
-    vis = visibility_rows(role, turn_id, r)
+    vis = visibility_rows(role, turn_id, r, nexus_scope=nexus_scope)
     g = kv_head(h, Hq, Hkv)
     scores = scale * (qf[r, h, :] @ kf[:, g, :].T)
     return softmax_probs(scores, vis)
 
 
 def prefill_request(q, k, v, role, turn_id, scale=None, rows=None, block=512,
-                    parsed: Parsed = None) -> np.ndarray:
+                    parsed: Parsed = None, nexus_scope: str = NEXUS_ALL) -> np.ndarray:
     """O[rows, Hq, d] for one request: dense scores, explicit mask, softmax, P @ V."""
     kf = bf16_bits_to_f64(k)
     vf = bf16_bits_to_f64(v)
@@ -73,7 +73,7 @@ def prefill_request(q, k, v, role, turn_id, scale=None, rows=None, block=512,
     for r0 in range(0, len(rows), block):
         rb = rows[r0:r0 + block]
         qf = bf16_bits_to_f64(q[rb])          # only the query rows of this block
-        vis = visibility_rows(role, turn_id, rb, parsed=parsed)
+        vis = visibility_rows(role, turn_id, rb, parsed=parsed, nexus_scope=nexus_scope)
         for h in range(Hq):
             g = kv_head(h, Hq, Hkv)
             scores = scale * (qf[:, h, :] @ kf[:, g, :].T)

@@ -12,7 +12,12 @@ the section states them:
   segment i (p > max(N_i)), every body key of B_i is masked.  Reading A4: a
   segment without Nexus tokens ends at its last body token.
 * Bidirectional Nexus visibility, Eq.(5): every Nexus token sees every Nexus
-  token, within and across segments (the literal "fully connected" reading).
+  token, within and across segments (the literal "fully connected" reading,
+  scope NEXUS_ALL).  Reading A3' (scope NEXUS_UP_TO_OWN): a Nexus token sees
+  the Nexus tokens of its own segment and of the earlier ones, not of later
+  segments.  That is what a session computes when each segment's Nexus tokens
+  are generated as its turn ends, over the Nexus KV kept from the earlier
+  turns (the efficiency discussion of the paper keeps that KV across turns).
 
 Large requests are handled one block of query rows at a time; every block is
 still an explicit boolean matrix.
@@ -22,6 +27,9 @@ from __future__ import annotations
 import numpy as np
 
 from .layout import NEXUS, HISTORY_TEXT, Parsed, parse
+
+NEXUS_ALL = "all"              # Eq.(5) as written
+NEXUS_UP_TO_OWN = "up_to_own"  # reading A3': own and earlier segments only
 
 
 def _last_of_key(parsed: Parsed) -> np.ndarray:
@@ -33,7 +41,15 @@ def _last_of_key(parsed: Parsed) -> np.ndarray:
     return last
 
 
-def visibility_rows(role, turn_id, rows=None, parsed: Parsed = None) -> np.ndarray:
+def _nexus_segment(parsed: Parsed) -> np.ndarray:
+    """Segment index (0, 1, ...) of each Nexus position; -1 elsewhere."""
+    seg = np.full(parsed.length, -1, dtype=np.int64)
+    for i, s in enumerate(parsed.segments):
+        seg[s.nexus_start:s.nexus_start + s.nexus_len] = i
+    return seg
+
+
+def visibility_rows(role, turn_id, rows=None, parsed: Parsed = None, nexus_scope: str = NEXUS_ALL) -> np.ndarray:
     """Boolean visibility of all L keys for the query positions `rows` (default: all)."""
     role = np.asarray(role)
     if parsed is None:
@@ -54,17 +70,24 @@ def visibility_rows(role, turn_id, rows=None, parsed: Parsed = None) -> np.ndarr
     # Eq.(4): p > max(N_i) masks the body B_i
     last = _last_of_key(parsed)[None, :]
     vis &= ~(body_q & (P > last))
-    # Eq.(5): Nexus <-> Nexus fully visible, within and across segments
-    vis |= nexus_p & nexus_q
+    # Eq.(5): Nexus <-> Nexus fully visible, within and across segments (A3' limits
+    # the keys to the query's own and earlier segments)
+    if nexus_scope == NEXUS_ALL:
+        vis |= nexus_p & nexus_q
+    elif nexus_scope == NEXUS_UP_TO_OWN:
+        seg = _nexus_segment(parsed)
+        vis |= nexus_p & nexus_q & (seg[None, :] <= seg[p][:, None])
+    else:
+        raise ValueError(f"unknown Nexus scope {nexus_scope!r}")
     return vis
 
 
-def visibility(role, turn_id) -> np.ndarray:
+def visibility(role, turn_id, nexus_scope: str = NEXUS_ALL) -> np.ndarray:
     """The full explicit L x L boolean mask of one request."""
-    return visibility_rows(role, turn_id)
+    return visibility_rows(role, turn_id, nexus_scope=nexus_scope)
 
 
-def additive_mask(role, turn_id) -> np.ndarray:
+def additive_mask(role, turn_id, nexus_scope: str = NEXUS_ALL) -> np.ndarray:
     """M itself: 0 where visible, -inf where masked (float64)."""
-    vis = visibility(role, turn_id)
+    vis = visibility(role, turn_id, nexus_scope)
     return np.where(vis, 0.0, -np.inf)

@@ -25,7 +25,9 @@ def segment_sets(role, turn):
     return [(b, n) for b, n, _ in sets]
 
 
-def brute_force_mask(role, turn):
+def brute_force_mask(role, turn, nexus_scope="all"):
+    """nexus_scope "all": Eq.(5) as written; "up_to_own": a Nexus query sees the Nexus
+    keys of its own and earlier segments only (reading A3')."""
     L = len(role)
     M = [[NEG] * L for _ in range(L)]
     # Basic causal rule, Eq.(3); applied globally, so mixed text/Nexus pairs too.
@@ -42,23 +44,29 @@ def brute_force_mask(role, turn):
                 for q in body:
                     M[p][q] = NEG
     # Bidirectional Nexus visibility, Eq.(5).
+    seg_of = {}
+    for i, (_, nexus) in enumerate(segment_sets(role, turn)):
+        for p in nexus:
+            seg_of[p] = i
     all_nexus = [p for p in range(L) if role[p] == NEXUS]
     for a in all_nexus:
         for b in all_nexus:
-            M[a][b] = 0.0
+            if nexus_scope == "all" or seg_of[b] <= seg_of[a]:
+                M[a][b] = 0.0
     return [[M[p][q] == 0.0 for q in range(L)] for p in range(L)]
 
 
-def closed_form_row_counts(system, bodies, nexus, current):
+def closed_form_row_counts(system, bodies, nexus, current, nexus_scope="all"):
     """Visible keys per query row, derived by hand from the rules for a well-formed layout:
     system row r -> r+1; body row r of segment i -> S + P_i + r + 1 (P_i = Nexus before i);
-    Nexus row of segment i -> S + b_i + K_tot; current row r -> S + K_tot + r + 1."""
+    Nexus row of segment i -> S + b_i + K_tot (under "up_to_own": S + b_i + P_i + k_i);
+    current row r -> S + K_tot + r + 1."""
     counts = [r + 1 for r in range(system)]
     K_tot = sum(nexus)
     P = 0
     for b, k in zip(bodies, nexus):
         counts += [system + P + r + 1 for r in range(b)]
-        counts += [system + b + K_tot] * k
+        counts += [system + b + (K_tot if nexus_scope == "all" else P + k)] * k
         P += k
     counts += [system + K_tot + r + 1 for r in range(current)]
     return counts

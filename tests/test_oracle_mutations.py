@@ -85,8 +85,8 @@ def test_ending_segment_at_its_body_is_caught(monkeypatch):
 def test_nexus_visibility_only_within_segment_is_caught(monkeypatch):
     real = OM.visibility_rows
 
-    def within_segment_only(role, turn_id, rows=None, parsed=None):
-        vis = real(role, turn_id, rows, parsed)
+    def within_segment_only(role, turn_id, rows=None, parsed=None, nexus_scope=OM.NEXUS_ALL):
+        vis = real(role, turn_id, rows, parsed, nexus_scope)
         role = np.asarray(role)
         turn_id = np.asarray(turn_id)
         p = np.arange(len(role)) if rows is None else np.asarray(rows)
@@ -124,3 +124,33 @@ def test_keys_used_as_values_is_caught(monkeypatch):
         return out
     monkeypatch.setattr(OA, "bf16_bits_to_f64", swap_third)
     assert not _causal_pin_holds()
+
+
+def _up_to_own_pin_holds():
+    rng = np.random.default_rng(59)
+    for _ in range(40):
+        lay = W.random_layout(rng, max_h=3, max_b=4, max_k=3, max_s=2, max_c=2)
+        role, turn = lay.roles_and_turns()
+        got = OM.visibility(role, turn, OM.NEXUS_UP_TO_OWN)
+        want = np.array(brute.brute_force_mask(role.tolist(), turn.tolist(), "up_to_own"),
+                        dtype=bool).reshape(got.shape)
+        if not np.array_equal(got, want):
+            return False
+    return True
+
+
+def test_up_to_own_pin_holds_unmutated():
+    assert _up_to_own_pin_holds()
+
+
+def test_up_to_own_seeing_every_segment_is_caught(monkeypatch):
+    """Reading A3' collapsed back to Eq.(5) as written (one segment index for all)."""
+    monkeypatch.setattr(OM, "_nexus_segment", lambda parsed: np.zeros(parsed.length, dtype=np.int64))
+    assert not _up_to_own_pin_holds()
+
+
+def test_up_to_own_reversed_segment_order_is_caught(monkeypatch):
+    """Later segments seen instead of earlier ones."""
+    real = OM._nexus_segment
+    monkeypatch.setattr(OM, "_nexus_segment", lambda parsed: -real(parsed))
+    assert not _up_to_own_pin_holds()
