@@ -75,6 +75,23 @@ enum {
     SONIC_ROLE_CURRENT = 3       /* Q_curr, and every generated token                */
 };
 
+/*
+ * Scope of Nexus <-> Nexus visibility in the prefill mask.
+ *   SONIC_NEXUS_ALL        Eq.(5) as written: every Nexus token sees every Nexus
+ *                          token of the request, within and across segments.
+ *   SONIC_NEXUS_UP_TO_OWN  a Nexus token sees the Nexus tokens of its own segment
+ *                          and of the earlier ones only.  This is what a session
+ *                          computes when each segment's Nexus tokens are made as
+ *                          its turn ends, over the Nexus KV kept from the earlier
+ *                          turns (sonic_nexus_extend); a full prefill with this
+ *                          scope reproduces those rows.
+ * Every other rule of the mask is the same under both.
+ */
+enum {
+    SONIC_NEXUS_ALL = 0,
+    SONIC_NEXUS_UP_TO_OWN = 1
+};
+
 /* Version of this ABI (bumped on any signature or layout change). */
 int32_t sonic_abi_version(void);
 
@@ -97,12 +114,15 @@ int32_t sonic_validate_layout_host(int32_t batch, const int32_t *cu_seqlens, con
 /*
  * Per-request work figures of a well-formed batch, on the CPU:
  *   visible_pairs[b] - number of (query, key) pairs the mask of Sec. 3.2 leaves
- *                      visible; prefill does 4*d flops per pair and q-head;
+ *                      visible under nexus_scope (SONIC_NEXUS_*); prefill does
+ *                      4*d flops per pair and q-head;
  *   kept_rows[b]     - rows retained by compaction (system + Nexus + current).
- * Either output may be NULL.  Returns SONIC_ERR_BAD_LAYOUT on a grammar error.
+ * Either output may be NULL.  Returns SONIC_ERR_BAD_LAYOUT on a grammar error,
+ * SONIC_ERR_INVALID_ARG for an unknown scope.
  */
 int32_t sonic_layout_stats_host(int32_t batch, const int32_t *cu_seqlens, const uint8_t *role,
-                                const int32_t *turn_id, int64_t *visible_pairs, int32_t *kept_rows);
+                                const int32_t *turn_id, int32_t nexus_scope, int64_t *visible_pairs,
+                                int32_t *kept_rows);
 
 /* ------------------------------------------------------------------------ */
 /* Step 1: masked prefill attention                                          */
@@ -121,8 +141,9 @@ size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens, int32_
  * out[p][h] = sum_q softmax_q(scale * <q[p][h], k[q][g(h)]> + M[p][q]) * v[q][g(h)]
  * for every token p of every request, where M is the hierarchical visibility
  * mask of Sec. 3.2: causal (Eq.(3), applied globally), history bodies removed
- * for every position after their segment's last Nexus token (Eq.(4)), and all
- * Nexus tokens mutually visible within and across segments (Eq.(5)).
+ * for every position after their segment's last Nexus token (Eq.(4)), and
+ * Nexus tokens mutually visible (Eq.(5)): all of them under SONIC_NEXUS_ALL,
+ * those of the own and earlier segments under SONIC_NEXUS_UP_TO_OWN.
  * Fully masked key blocks are never visited: the kernels enumerate the visible
  * keys of each block of query rows from the segment structure.
  *
@@ -133,6 +154,7 @@ size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens, int32_
  *   role, turn_id         device uint8 [T], int32 [T]
  *   q                     device bf16 [T][Hq][d];  k, v: device bf16 [T][Hkv][d]
  *   softmax_scale         finite and > 0, e.g. 1/sqrt(d)
+ *   nexus_scope           SONIC_NEXUS_ALL or SONIC_NEXUS_UP_TO_OWN
  *   out                   device fp32 [T][Hq][d] (fully written on success)
  *   workspace             device, >= sonic_prefill_workspace_bytes(B, T, Hkv, d) bytes,
  *                         256-byte aligned; contents need no initialisation
@@ -144,8 +166,8 @@ size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens, int32_
 int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t num_q_heads,
                                    int32_t num_kv_heads, int32_t head_dim, const int32_t *cu_seqlens,
                                    const uint8_t *role, const int32_t *turn_id, const void *q, const void *k,
-                                   const void *v, float softmax_scale, float *out, void *workspace,
-                                   size_t workspace_bytes, int32_t *dev_status, void *stream);
+                                   const void *v, float softmax_scale, int32_t nexus_scope, float *out,
+                                   void *workspace, size_t workspace_bytes, int32_t *dev_status, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Step 2: KV compaction                                                     */

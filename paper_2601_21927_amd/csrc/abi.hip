@@ -9,7 +9,7 @@
 #include "common.h"
 
 namespace sonic {
-hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus, const int32_t *cu,
+hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus, int nexus_scope, const int32_t *cu,
                        const uint8_t *role, const int32_t *turn, const uint16_t *k, const uint16_t *v, PrefillWs ws,
                        int32_t *status, hipStream_t stream);
 hipError_t prefill_occupancy(int D, int G, int *blocks);
@@ -35,7 +35,7 @@ hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int nsp
 
 namespace {
 
-constexpr int kAbiVersion = 3;
+constexpr int kAbiVersion = 4;
 constexpr double kLog2e = 1.4426950408889634;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -173,7 +173,8 @@ int32_t sonic_validate_layout_host(int32_t batch, const int32_t *cu, const uint8
 }
 
 int32_t sonic_layout_stats_host(int32_t batch, const int32_t *cu, const uint8_t *role, const int32_t *turn_id,
-                                int64_t *visible_pairs, int32_t *kept_rows) {
+                                int32_t nexus_scope, int64_t *visible_pairs, int32_t *kept_rows) {
+  if (nexus_scope != SONIC_NEXUS_ALL && nexus_scope != SONIC_NEXUS_UP_TO_OWN) return SONIC_ERR_INVALID_ARG;
   int32_t bad = -1;
   const int32_t st = sonic_validate_layout_host(batch, cu, role, turn_id, &bad);
   if (st != SONIC_OK) return st;
@@ -184,12 +185,14 @@ int32_t sonic_layout_stats_host(int32_t batch, const int32_t *cu, const uint8_t 
     int64_t k_tot = 0;
     for (const HostSeg &s : hp.segs) k_tot += s.nexus_len;
     // system rows: causal; body row r of segment i: S + (Nexus before i) + r + 1;
-    // Nexus row of segment i: S + b_i + K_tot; current row r: S + K_tot + r + 1.
+    // Nexus row of segment i: S + b_i + K_tot (own and earlier segments only:
+    // S + b_i + (Nexus before i) + k_i); current row r: S + K_tot + r + 1.
     int64_t pairs = S * (S + 1) / 2 + C * (S + k_tot) + C * (C + 1) / 2;
     int64_t before = 0;
     for (const HostSeg &s : hp.segs) {
       const int64_t bl = s.body_len, kl = s.nexus_len;
-      pairs += bl * (S + before) + bl * (bl + 1) / 2 + kl * (S + bl + k_tot);
+      const int64_t nexus_keys = nexus_scope == SONIC_NEXUS_ALL ? k_tot : before + kl;
+      pairs += bl * (S + before) + bl * (bl + 1) / 2 + kl * (S + bl + nexus_keys);
       before += kl;
     }
     if (visible_pairs) visible_pairs[b] = pairs;
@@ -239,10 +242,12 @@ size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens, int32_
 
 int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t Hq, int32_t Hkv, int32_t d,
                                    const int32_t *cu_seqlens, const uint8_t *role, const int32_t *turn_id,
-                                   const void *q, const void *k, const void *v, float softmax_scale, float *out,
-                                   void *workspace, size_t workspace_bytes, int32_t *dev_status, void *stream_) {
+                                   const void *q, const void *k, const void *v, float softmax_scale,
+                                   int32_t nexus_scope, float *out, void *workspace, size_t workspace_bytes,
+                                   int32_t *dev_status, void *stream_) {
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   if (batch < 0 || total_tokens < 0 || Hq <= 0 || Hkv <= 0 || dev_status == nullptr) return SONIC_ERR_INVALID_ARG;
+  if (nexus_scope != SONIC_NEXUS_ALL && nexus_scope != SONIC_NEXUS_UP_TO_OWN) return SONIC_ERR_INVALID_ARG;
   if (d != 64 && d != 128) return SONIC_ERR_UNSUPPORTED;
   if (Hq % Hkv != 0) return SONIC_ERR_INVALID_ARG;
   const int G = Hq / Hkv;
@@ -261,7 +266,7 @@ int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t 
   DeviceInfo *di = nullptr;
   hipError_t e = device_info(&di);
   if (e != hipSuccess) return SONIC_ERR_HIP;
-  e = launch_plan(batch, total_tokens, Hkv, d, di->num_cus, cu_seqlens, role, turn_id,
+  e = launch_plan(batch, total_tokens, Hkv, d, di->num_cus, nexus_scope, cu_seqlens, role, turn_id,
                   static_cast<const uint16_t *>(k), static_cast<const uint16_t *>(v), ws, dev_status, stream);
   if (e != hipSuccess) return SONIC_ERR_HIP;
   int grid = di->num_cus * di->prefill_blocks[d == 128][G];

@@ -7,7 +7,9 @@
 //     earlier segments (causal; A1), and its own body up to itself; earlier
 //     bodies are removed because the row lies after their segment (Eq.(4));
 //   * a Nexus row of segment i sees the system prompt, its own body (it is not
-//     after max(N_i)) and every Nexus token of the request (Eq.(5));
+//     after max(N_i)) and every Nexus token of the request (Eq.(5)), or, with the
+//     narrower Nexus scope, those of segments 1..i only: a shorter leading part
+//     of the same prefix;
 //   * a current-query row sees the system prompt, every Nexus token and the
 //     current query up to itself; all bodies are removed (Eq.(4)).
 // Every block of at most 32 rows of one run therefore sees the same key list
@@ -59,7 +61,8 @@ __device__ __forceinline__ bool legal_step(int rp, int tp, int r, int t) {
 __global__ __launch_bounds__(kPlanThreads) void plan_runs_kernel(const int32_t *__restrict__ cu,
                                                                  const uint8_t *__restrict__ role,
                                                                  const int32_t *__restrict__ turn, PrefillWs ws,
-                                                                 int total_tokens, int32_t *status) {
+                                                                 int total_tokens, int nexus_scope,
+                                                                 int32_t *status) {
   __shared__ int lds[kPlanThreads / kWave + 1];
   __shared__ int s_bad;
   __shared__ unsigned long long s_cost;
@@ -160,8 +163,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_runs_kernel(const int32_t *
           d.seg_start = start;
           d.seg_len = d.p0 + d.nrows - start;
           d.ndiag = d.nrows;
-        } else if (kind == kNexus) {    // system + every Nexus, the owning body
-          d.npre = npre_all;
+        } else if (kind == kNexus) {    // system + every Nexus (or up to its own), the owning body
+          d.npre = nexus_scope == SONIC_NEXUS_ALL ? npre_all : pre_before + (end - start);
           d.seg_start = body_start;
           d.seg_len = body_len;
           d.ndiag = 0;
@@ -288,10 +291,11 @@ hipError_t launch_plan_order(int batch, const int32_t *cu, PrefillWs ws, int32_t
   return hipGetLastError();
 }
 
-hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus, const int32_t *cu,
+hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus, int nexus_scope, const int32_t *cu,
                        const uint8_t *role, const int32_t *turn, const uint16_t *k, const uint16_t *v, PrefillWs ws,
                        int32_t *status, hipStream_t stream) {
-  plan_runs_kernel<<<dim3(batch), dim3(kPlanThreads), 0, stream>>>(cu, role, turn, ws, total_tokens, status);
+  plan_runs_kernel<<<dim3(batch), dim3(kPlanThreads), 0, stream>>>(cu, role, turn, ws, total_tokens, nexus_scope,
+                                                                    status);
   hipError_t e = launch_plan_order(batch, cu, ws, status, stream);
   if (e != hipSuccess) return e;
   const int row_pieces = Hkv * D / 8;

@@ -60,9 +60,9 @@ class SonicBatch:
         self.cache = None
 
     # ------------------------------------------------------------- step 1
-    def prefill(self, stream=None) -> int:
+    def prefill(self, stream=None, nexus_scope: int = sonic.NEXUS_ALL) -> int:
         return sonic.segment_attn_prefill(self.cu, self.role, self.turn_id, self.q, self.k, self.v, self.out,
-                                          self.prefill_ws, self.status, stream=stream)
+                                          self.prefill_ws, self.status, nexus_scope=nexus_scope, stream=stream)
 
     # ------------------------------------------------------------- step 2
     def alloc_cache(self, capacities: Sequence[int], fill_bits: int = 0xFFFF):

@@ -26,6 +26,7 @@ ERR_UNSUPPORTED = 5
 ERR_HIP = 6
 
 ROLE_SYSTEM, ROLE_HISTORY_TEXT, ROLE_NEXUS, ROLE_CURRENT = 0, 1, 2, 3
+NEXUS_ALL, NEXUS_UP_TO_OWN = 0, 1   # Nexus <-> Nexus visibility scope of the prefill mask
 
 EXPORTS = (
     "sonic_abi_version", "sonic_status_string", "sonic_validate_layout_host", "sonic_layout_stats_host",
@@ -60,12 +61,12 @@ def lib() -> ctypes.CDLL:
     L.sonic_validate_layout_host.restype = _i32
     L.sonic_validate_layout_host.argtypes = [_i32, _p, _p, _p, _p]
     L.sonic_layout_stats_host.restype = _i32
-    L.sonic_layout_stats_host.argtypes = [_i32, _p, _p, _p, _p, _p]
+    L.sonic_layout_stats_host.argtypes = [_i32, _p, _p, _p, _i32, _p, _p]
     L.sonic_prefill_workspace_bytes.restype = _sz
     L.sonic_prefill_workspace_bytes.argtypes = [_i32, _i32, _i32, _i32]
     L.sonic_segment_attn_prefill.restype = _i32
-    L.sonic_segment_attn_prefill.argtypes = [_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _f32, _p, _p,
-                                             _sz, _p, _p]
+    L.sonic_segment_attn_prefill.argtypes = [_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _f32, _i32, _p,
+                                             _p, _sz, _p, _p]
     L.sonic_kv_compact.restype = _i32
     L.sonic_kv_compact.argtypes = [_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p]
     L.sonic_decode_workspace_bytes.restype = _sz
@@ -135,7 +136,7 @@ def validate_layout_host(cu_seqlens, role, turn_id):
     return int(st), int(bad.value)
 
 
-def layout_stats_host(cu_seqlens, role, turn_id):
+def layout_stats_host(cu_seqlens, role, turn_id, nexus_scope: int = NEXUS_ALL):
     """(visible pairs per request int64[B], kept rows per request int32[B])."""
     import numpy as np
     cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
@@ -144,7 +145,8 @@ def layout_stats_host(cu_seqlens, role, turn_id):
     B = len(cu) - 1
     vis = np.zeros(max(B, 1), np.int64)
     kept = np.zeros(max(B, 1), np.int32)
-    st = lib().sonic_layout_stats_host(B, _np_ptr(cu), _np_ptr(r), _np_ptr(t), _np_ptr(vis), _np_ptr(kept))
+    st = lib().sonic_layout_stats_host(B, _np_ptr(cu), _np_ptr(r), _np_ptr(t), int(nexus_scope), _np_ptr(vis),
+                                       _np_ptr(kept))
     if st != OK:
         raise SonicError(st, "sonic_layout_stats_host")
     return vis[:B], kept[:B]
@@ -156,7 +158,7 @@ def prefill_workspace_bytes(batch: int, total_tokens: int, num_kv_heads: int, he
 
 
 def segment_attn_prefill(cu_seqlens, role, turn_id, q, k, v, out, workspace, dev_status, softmax_scale=None,
-                         stream=None) -> int:
+                         nexus_scope: int = NEXUS_ALL, stream=None) -> int:
     """q [T,Hq,d] bf16, k/v [T,Hkv,d] bf16, out [T,Hq,d] fp32; cu int32 [B+1]; role uint8 [T];
     turn_id int32 [T]; workspace uint8 [>= prefill_workspace_bytes]; dev_status int32 [1]."""
     _dev(cu_seqlens, role, turn_id, q, k, v, out, workspace, dev_status)
@@ -167,7 +169,7 @@ def segment_attn_prefill(cu_seqlens, role, turn_id, q, k, v, out, workspace, dev
     scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
     return int(lib().sonic_segment_attn_prefill(
         cu_seqlens.numel() - 1, T, Hq, Hkv, d, _ptr(cu_seqlens), _ptr(role), _ptr(turn_id), _ptr(q), _ptr(k),
-        _ptr(v), scale, _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _ptr(v), scale, int(nexus_scope), _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(),
         _ptr(dev_status), _stream(stream)))
 
 

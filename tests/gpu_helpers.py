@@ -10,6 +10,7 @@ from oracle import attention as OA
 from oracle import compaction as OC
 from oracle import decode as OD
 from oracle import layout as OL
+from oracle import mask as OM
 
 # Attention tolerance for bf16 inputs with fp32 accumulation, against the fp64 oracle.
 MAX_ABS = 1e-2
@@ -57,7 +58,7 @@ def sample_rows(lay: W.RequestLayout, rng, every=None, extra=16):
     return np.array(sorted(rows), np.int64)
 
 
-def oracle_prefill_rows(batch: W.Batch, rows_per_req):
+def oracle_prefill_rows(batch: W.Batch, rows_per_req, nexus_scope=OM.NEXUS_ALL):
     outs = []
     cu = batch.cu_seqlens
     for b, rows in enumerate(rows_per_req):
@@ -66,7 +67,7 @@ def oracle_prefill_rows(batch: W.Batch, rows_per_req):
             outs.append(np.zeros((0, batch.num_q_heads, batch.head_dim)))
             continue
         outs.append(OA.prefill_request(batch.q[s:e], batch.k[s:e], batch.v[s:e], batch.role[s:e],
-                                       batch.turn_id[s:e], rows=rows))
+                                       batch.turn_id[s:e], rows=rows, nexus_scope=nexus_scope))
     return outs
 
 

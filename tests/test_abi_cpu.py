@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert sonic.abi_version() == 3
+    assert sonic.abi_version() == 4
     assert sonic.status_string(0) == "ok"
     for code in range(1, 7):
         assert sonic.status_string(code) != "unknown status"
@@ -100,6 +100,18 @@ def test_layout_stats_match_oracle_mask_counts():
         r, t = lay.roles_and_turns()
         assert vis[b] == int(OM.visibility(r, t).sum())
         assert kept[b] == int(np.sum(r != OL.HISTORY_TEXT))
+
+
+def test_layout_stats_up_to_own_scope_match_oracle_mask_counts():
+    rng = np.random.default_rng(73)
+    lays = [W.random_layout(rng) for _ in range(40)]
+    cu, role, turn = _pack(lays)
+    vis, _ = sonic.layout_stats_host(cu, role, turn, sonic.NEXUS_UP_TO_OWN)
+    for b, lay in enumerate(lays):
+        r, t = lay.roles_and_turns()
+        assert vis[b] == int(OM.visibility(r, t, OM.NEXUS_UP_TO_OWN).sum())
+    with pytest.raises(sonic.SonicError):
+        sonic.layout_stats_host(cu, role, turn, 7)
 
 
 @pytest.mark.parametrize("idx,pairs", [(1, 50736), (2, 5194240), (4, 193692160)])

@@ -11,18 +11,18 @@ from tests import gpu_helpers as H
 pytestmark = pytest.mark.gpu
 
 
-def run_prefill(batch):
+def run_prefill(batch, nexus_scope=sonic.NEXUS_ALL):
     H.need_gpu()
     db = H.device_batch(batch)
     db.out.fill_(float("nan"))
-    st = db.prefill()
+    st = db.prefill(nexus_scope=nexus_scope)
     assert st == sonic.OK, sonic.status_string(st)
     torch.cuda.synchronize()
     assert db.read_status() == 0, sonic.status_string(db.read_status())
     return db
 
 
-def check_all_rows(batch, db):
+def check_all_rows(batch, db, nexus_scope=OM.NEXUS_ALL):
     out = db.out.cpu().numpy()
     cu = batch.cu_seqlens
     for b, lay in enumerate(batch.layouts):
@@ -30,7 +30,7 @@ def check_all_rows(batch, db):
         if e == s:
             continue
         want = H.oracle_prefill_rows(batch, [np.arange(e - s) if i == b else np.zeros(0, np.int64)
-                                             for i in range(batch.batch)])[b]
+                                             for i in range(batch.batch)], nexus_scope)[b]
         H.assert_close(out[s:e], want, f"{batch.name} request {b} (L={e - s})")
 
 
@@ -70,7 +70,49 @@ def test_prefill_edge_layouts(name):
     check_all_rows(batch, db)
 
 
-def test_prefill_mask_revealed_by_one_hot_values():
+@pytest.mark.parametrize("Hq,Hkv,d", [(4, 2, 64), (32, 8, 128), (7, 1, 128)])
+def test_prefill_up_to_own_scope_random_layouts_all_rows(Hq, Hkv, d):
+    """Nexus rows see the Nexus tokens of their own and earlier segments only."""
+    rng = np.random.default_rng(500 + Hq * 7 + Hkv + d)
+    lays = [W.random_layout(rng, max_h=5, max_b=90, max_k=45, max_s=70, max_c=70) for _ in range(3)]
+    lays.append(W.RequestLayout(3, [40, 2, 33], [33, 1, 64], 5))
+    H.note(f"prefill up-to-own scope Hq={Hq} Hkv={Hkv} d={d}: {[l.length for l in lays]}")
+    batch = W.make_batch("scope", lays, Hq, Hkv, d, seed=int(rng.integers(1 << 30)))
+    db = run_prefill(batch, sonic.NEXUS_UP_TO_OWN)
+    check_all_rows(batch, db, OM.NEXUS_UP_TO_OWN)
+
+
+def test_prefill_up_to_own_scope_workload_rows():
+    """The 8B-shaped workload: every Nexus row of segments 1, 4 and 8 and sampled other rows."""
+    H.need_gpu()
+    batch = W.workload(2, decode_steps=0)
+    db = run_prefill(batch, sonic.NEXUS_UP_TO_OWN)
+    out = db.out.cpu().numpy()
+    rng = np.random.default_rng(5)
+    lay = batch.layouts[0]
+    nexus_rows = []
+    p = lay.system
+    for i, (bl, k) in enumerate(zip(lay.bodies, lay.nexus)):
+        if i in (0, 3, 7):
+            nexus_rows.append(np.arange(p + bl, p + bl + k))
+        p += bl + k
+    rows = [np.unique(np.concatenate(nexus_rows + [rng.integers(0, lay.length, 24)])) if b in (0, 5) else
+            np.zeros(0, np.int64) for b in range(batch.batch)]
+    want = H.oracle_prefill_rows(batch, rows, OM.NEXUS_UP_TO_OWN)
+    for b in (0, 5):
+        s = int(batch.cu_seqlens[b])
+        H.assert_close(out[s + rows[b]], want[b], f"workload 2 up-to-own request {b}")
+
+
+def test_prefill_unknown_scope_is_rejected():
+    H.need_gpu()
+    batch = W.make_batch("scope-arg", [W.RequestLayout(3, [5], [2], 2)], 4, 2, 64, seed=1)
+    db = H.device_batch(batch)
+    assert db.prefill(nexus_scope=2) == sonic.ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("scope", [OM.NEXUS_ALL, OM.NEXUS_UP_TO_OWN])
+def test_prefill_mask_revealed_by_one_hot_values(scope):
     """Q = 0 and V[q] = e_q make output row p equal 1/|vis(p)| on exactly the visible keys."""
     H.need_gpu()
     lays = [W.RequestLayout(5, [20, 17, 9], [7, 0, 12], 17), W.RequestLayout(0, [40], [3], 30)]
@@ -84,12 +126,12 @@ def test_prefill_mask_revealed_by_one_hot_values():
         for i in range(lay.length):
             v[s + i, :, i] = 0x3F80   # 1.0
     batch.v = v
-    db = run_prefill(batch)
+    db = run_prefill(batch, sonic.NEXUS_ALL if scope == OM.NEXUS_ALL else sonic.NEXUS_UP_TO_OWN)
     out = db.out.cpu().numpy()
     for b, lay in enumerate(lays):
         s, e = int(batch.cu_seqlens[b]), int(batch.cu_seqlens[b + 1])
         role, turn = lay.roles_and_turns()
-        vis = OM.visibility(role, turn)
+        vis = OM.visibility(role, turn, scope)
         L = e - s
         for p in range(L):
             n = int(vis[p].sum())
