@@ -24,9 +24,13 @@ those definitions out, slowly and in float64:
 * ``extend``     - the next turn's Nexus rows over the compact cache (Sec. 3.2
                    mask restricted to the newest segment) and the cache update
                    that drops the turn's body and keeps its Nexus KV.
+* ``stats``      - attention statistics behind the training objectives of
+                   Sec. 4: the Nexus attention mass per query row and head, and
+                   the head-averaged attention each key receives from the
+                   current rows.
 
 Inputs are bf16 bit patterns (uint16); they are widened exactly to float64.
 """
-from . import layout, mask, attention, compaction, decode, extend  # noqa: F401
+from . import layout, mask, attention, compaction, decode, extend, stats  # noqa: F401
 
-__all__ = ["layout", "mask", "attention", "compaction", "decode", "extend"]
+
