@@ -212,6 +212,17 @@ def main():
         torch.cuda.synchronize()
         return a.elapsed_time(b_) / n
     pf_b2b_ms = back_to_back("prefill", 10)
+    # the same prefill with both attention statistics (Nexus mass per row and head, key weights)
+    stat_mass = torch.empty((batch.total_tokens, Hq), dtype=torch.float32, device=dev)
+    stat_w = torch.empty((batch.total_tokens,), dtype=torch.float32, device=dev)
+
+    def run_prefill_stats():
+        st = db.prefill(nexus_mass=stat_mass, key_weight=stat_w)
+        assert st == sonic.OK, sonic.status_string(st)
+    phases["prefill_stats"] = run_prefill_stats
+    run_prefill_stats()
+    torch.cuda.synchronize()
+    pfs_b2b_ms = back_to_back("prefill_stats", 10)
     cp_b2b_ms = back_to_back("compact", 20)
     assert db.read_status() == 0
 
@@ -327,6 +338,7 @@ def main():
             "compact_frac_hbm_peak": round(compact_gbs / PEAK_HBM_GBS, 4),
             "prefill_ms_back_to_back": round(pf_b2b_ms, 4),
             "prefill_visible_tflops_back_to_back": round(visible_flops / (pf_b2b_ms * 1e-3) / 1e12, 2),
+            "prefill_with_statistics_ms_back_to_back": round(pfs_b2b_ms, 4),
             "compact_us_back_to_back": round(cp_b2b_ms * 1e3, 2),
             "compact_gbs_back_to_back": round(compact_bytes / (cp_b2b_ms * 1e-3) / 1e9, 1),
             "decode_ms_256_steps": round(dc_ms, 4), "decode_us_per_step": round(dc_ms * 1e3 / steps_dec, 2),

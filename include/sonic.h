@@ -131,11 +131,13 @@ int32_t sonic_layout_stats_host(int32_t batch, const int32_t *cu_seqlens, const 
 /*
  * Bytes of device workspace sonic_segment_attn_prefill needs for this batch
  * (0 for negative sizes or non-positive heads / head_dim).  It holds the
- * per-block plan and a copy of each request's system and Nexus K/V rows, so
- * it grows as total_tokens * num_kv_heads * head_dim * 4 bytes.
+ * per-block plan, a copy of each request's system and Nexus K/V rows, and the
+ * buffers of the attention statistics, so it grows as
+ * total_tokens * (num_kv_heads * head_dim * 4 + (num_q_heads + num_kv_heads) * 4)
+ * bytes.
  */
-size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens, int32_t num_kv_heads,
-                                     int32_t head_dim);
+size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens, int32_t num_q_heads,
+                                     int32_t num_kv_heads, int32_t head_dim);
 
 /*
  * out[p][h] = sum_q softmax_q(scale * <q[p][h], k[q][g(h)]> + M[p][q]) * v[q][g(h)]
@@ -156,7 +158,19 @@ size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens, int32_
  *   softmax_scale         finite and > 0, e.g. 1/sqrt(d)
  *   nexus_scope           SONIC_NEXUS_ALL or SONIC_NEXUS_UP_TO_OWN
  *   out                   device fp32 [T][Hq][d] (fully written on success)
- *   workspace             device, >= sonic_prefill_workspace_bytes(B, T, Hkv, d) bytes,
+ *   nexus_mass            NULL, or device fp32 [T][Hq]: per row p and q-head h the
+ *                         attention mass on the request's Nexus keys,
+ *                         sum over Nexus keys x of softmax_x(...)[p][x] (the
+ *                         quantity the Nexus attention regulariser of Sec. 4
+ *                         averages over the current query)
+ *   key_weight            NULL, or device fp32 [T]: per key x the attention it
+ *                         receives from the CURRENT rows of its request, summed
+ *                         over those rows and averaged over the q-heads (the
+ *                         importance score of the attention-guided distillation
+ *                         of Sec. 4); 0 for history-body keys, which no current
+ *                         row sees.  Deterministic (no atomic sums).
+ *                         Either statistic costs a few percent of the prefill.
+ *   workspace             device, >= sonic_prefill_workspace_bytes(B, T, Hq, Hkv, d) bytes,
  *                         256-byte aligned; contents need no initialisation
  *   dev_status            device int32 (see conventions); SONIC_ERR_BAD_LAYOUT
  *                         is reported here and then no output is written
@@ -167,7 +181,8 @@ int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t 
                                    int32_t num_kv_heads, int32_t head_dim, const int32_t *cu_seqlens,
                                    const uint8_t *role, const int32_t *turn_id, const void *q, const void *k,
                                    const void *v, float softmax_scale, int32_t nexus_scope, float *out,
-                                   void *workspace, size_t workspace_bytes, int32_t *dev_status, void *stream);
+                                   float *nexus_mass, float *key_weight, void *workspace, size_t workspace_bytes,
+                                   int32_t *dev_status, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Step 2: KV compaction                                                     */

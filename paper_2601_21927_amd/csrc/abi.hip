@@ -12,7 +12,10 @@ namespace sonic {
 hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus, int nexus_scope, const int32_t *cu,
                        const uint8_t *role, const int32_t *turn, const uint16_t *k, const uint16_t *v, PrefillWs ws,
                        int32_t *status, hipStream_t stream);
-hipError_t prefill_occupancy(int D, int G, int *blocks);
+hipError_t prefill_occupancy(int D, int G, bool stats, int *blocks);
+hipError_t launch_key_weight(int batch, int T, int Hq, int Hkv, int D, int num_cus, const int32_t *cu,
+                             const uint8_t *role, const uint16_t *q, const uint16_t *k, PrefillWs ws,
+                             float scale_log2, float *w, int32_t *status, hipStream_t stream);
 hipError_t launch_plan_extend(int batch, int total_new, int max_rows, const int32_t *nexus_cu,
                               const int32_t *keep_len, const int32_t *cache_len, const int32_t *row_cap,
                               PrefillWs ws, int32_t *status, hipStream_t stream);
@@ -20,7 +23,7 @@ hipError_t launch_extend_append(int batch, int max_new, int Hkv, int D, const in
                                 const int32_t *keep_len, uint16_t *kc, uint16_t *vc, const int64_t *row_off,
                                 int32_t *cache_len, const uint16_t *k_new, const uint16_t *v_new,
                                 const int32_t *status, hipStream_t stream);
-hipError_t launch_prefill(int D, int G, int grid, AttnRows rows, PrefillWs ws, int Hkv, float scale_log2,
+hipError_t launch_prefill(int D, int G, int grid, bool stats, AttnRows rows, PrefillWs ws, int Hkv, float scale_log2,
                           hipStream_t stream);
 hipError_t launch_compact(int batch, int total_tokens, int max_seqlen, int Hkv, int D, const int32_t *cu,
                           const uint8_t *role,
@@ -35,7 +38,7 @@ hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int nsp
 
 namespace {
 
-constexpr int kAbiVersion = 4;
+constexpr int kAbiVersion = 5;
 constexpr double kLog2e = 1.4426950408889634;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -54,7 +57,7 @@ bool debug_sync() {
 struct DeviceInfo {
   bool valid = false;
   int num_cus = 0;
-  int prefill_blocks[2][9] = {};   // [D == 128][G]: resident workgroups per CU
+  int prefill_blocks[2][2][9] = {};   // [statistics variant][D == 128][G]: resident workgroups per CU
 };
 
 std::mutex g_dev_mutex;
@@ -70,13 +73,14 @@ hipError_t device_info(DeviceInfo **out) {
   if (!d.valid) {
     e = hipDeviceGetAttribute(&d.num_cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
-    for (int di = 0; di < 2; ++di)
-      for (int G = 1; G <= 8; ++G) {
-        int blocks = 0;
-        e = prefill_occupancy(di ? 128 : 64, G, &blocks);
-        if (e != hipSuccess) return e;
-        d.prefill_blocks[di][G] = blocks > 0 ? blocks : 1;
-      }
+    for (int st = 0; st < 2; ++st)
+      for (int di = 0; di < 2; ++di)
+        for (int G = 1; G <= 8; ++G) {
+          int blocks = 0;
+          e = prefill_occupancy(di ? 128 : 64, G, st != 0, &blocks);
+          if (e != hipSuccess) return e;
+          d.prefill_blocks[st][di][G] = blocks > 0 ? blocks : 1;
+        }
     d.valid = true;
   }
   *out = &d;
@@ -202,7 +206,8 @@ int32_t sonic_layout_stats_host(int32_t batch, const int32_t *cu, const uint8_t 
 }
 
 // ---------------------------------------------------------------- prefill
-static size_t prefill_ws_layout(int32_t batch, int32_t T, int32_t Hkv, int32_t d, PrefillWs *ws, char *base) {
+static size_t prefill_ws_layout(int32_t batch, int32_t T, int32_t Hq, int32_t Hkv, int32_t d, PrefillWs *ws,
+                                char *base) {
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -221,6 +226,11 @@ static size_t prefill_ws_layout(int32_t batch, int32_t T, int32_t Hkv, int32_t d
   const size_t rows_bytes = T1 * static_cast<size_t>(Hkv > 0 ? Hkv : 1) * static_cast<size_t>(d > 0 ? d : 1) * 2;
   char *kpre = take(rows_bytes);
   char *vpre = take(rows_bytes);
+  // attention statistics
+  char *lse = take(sizeof(float) * T1 * static_cast<size_t>(Hq > 0 ? Hq : 1));
+  char *wpart = take(sizeof(float) * T1 * static_cast<size_t>(Hkv > 0 ? Hkv : 1));
+  char *kblocks = take(sizeof(int2) * (T1 / 64 + B1 + 1));
+  char *ncur = take(sizeof(int32_t) * B1);
   if (ws) {
     ws->req = reinterpret_cast<ReqInfo *>(req);
     ws->req_off = reinterpret_cast<int32_t *>(req_off);
@@ -231,20 +241,25 @@ static size_t prefill_ws_layout(int32_t batch, int32_t T, int32_t Hkv, int32_t d
     ws->ctrl = reinterpret_cast<int32_t *>(ctrl);
     ws->k_pre = reinterpret_cast<uint16_t *>(kpre);
     ws->v_pre = reinterpret_cast<uint16_t *>(vpre);
+    ws->lse = reinterpret_cast<float *>(lse);
+    ws->wpart = reinterpret_cast<float *>(wpart);
+    ws->kblocks = reinterpret_cast<int2 *>(kblocks);
+    ws->ncur = reinterpret_cast<int32_t *>(ncur);
   }
   return off;
 }
 
-size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens, int32_t num_kv_heads, int32_t head_dim) {
-  if (batch < 0 || total_tokens < 0 || num_kv_heads <= 0 || head_dim <= 0) return 0;
-  return prefill_ws_layout(batch, total_tokens, num_kv_heads, head_dim, nullptr, nullptr);
+size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens, int32_t num_q_heads, int32_t num_kv_heads,
+                                     int32_t head_dim) {
+  if (batch < 0 || total_tokens < 0 || num_q_heads <= 0 || num_kv_heads <= 0 || head_dim <= 0) return 0;
+  return prefill_ws_layout(batch, total_tokens, num_q_heads, num_kv_heads, head_dim, nullptr, nullptr);
 }
 
 int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t Hq, int32_t Hkv, int32_t d,
                                    const int32_t *cu_seqlens, const uint8_t *role, const int32_t *turn_id,
                                    const void *q, const void *k, const void *v, float softmax_scale,
-                                   int32_t nexus_scope, float *out, void *workspace, size_t workspace_bytes,
-                                   int32_t *dev_status, void *stream_) {
+                                   int32_t nexus_scope, float *out, float *nexus_mass, float *key_weight,
+                                   void *workspace, size_t workspace_bytes, int32_t *dev_status, void *stream_) {
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   if (batch < 0 || total_tokens < 0 || Hq <= 0 || Hkv <= 0 || dev_status == nullptr) return SONIC_ERR_INVALID_ARG;
   if (nexus_scope != SONIC_NEXUS_ALL && nexus_scope != SONIC_NEXUS_UP_TO_OWN) return SONIC_ERR_INVALID_ARG;
@@ -255,13 +270,14 @@ int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t 
   if (!std::isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SONIC_ERR_INVALID_ARG;
   if (batch == 0 || total_tokens == 0) return SONIC_OK;
   if (!cu_seqlens || !role || !turn_id || !q || !k || !v || !out || !workspace) return SONIC_ERR_INVALID_ARG;
-  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) || !aligned(workspace, 256))
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) || !aligned(workspace, 256) ||
+      !aligned(nexus_mass, 4) || !aligned(key_weight, 4))
     return SONIC_ERR_INVALID_ARG;
   if (static_cast<size_t>(total_tokens) * Hq * d >= (size_t(1) << 40)) return SONIC_ERR_UNSUPPORTED;
   // K/V rows are addressed with 32-bit byte offsets inside one request
   if (static_cast<size_t>(total_tokens) * Hkv * d * 2 >= (size_t(1) << 32)) return SONIC_ERR_UNSUPPORTED;
   PrefillWs ws;
-  const size_t need = prefill_ws_layout(batch, total_tokens, Hkv, d, &ws, static_cast<char *>(workspace));
+  const size_t need = prefill_ws_layout(batch, total_tokens, Hq, Hkv, d, &ws, static_cast<char *>(workspace));
   if (workspace_bytes < need) return SONIC_ERR_WORKSPACE;
   DeviceInfo *di = nullptr;
   hipError_t e = device_info(&di);
@@ -269,11 +285,17 @@ int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t 
   e = launch_plan(batch, total_tokens, Hkv, d, di->num_cus, nexus_scope, cu_seqlens, role, turn_id,
                   static_cast<const uint16_t *>(k), static_cast<const uint16_t *>(v), ws, dev_status, stream);
   if (e != hipSuccess) return SONIC_ERR_HIP;
-  int grid = di->num_cus * di->prefill_blocks[d == 128][G];
+  const bool stats = nexus_mass != nullptr || key_weight != nullptr;
+  int grid = di->num_cus * di->prefill_blocks[stats][d == 128][G];
   grid = (grid + kNumXcd - 1) / kNumXcd * kNumXcd;
   AttnRows rows{cu_seqlens, nullptr, static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k),
-                static_cast<const uint16_t *>(v), ws.k_pre, ws.v_pre, out};
-  e = launch_prefill(d, G, grid, rows, ws, Hkv, static_cast<float>(softmax_scale * kLog2e), stream);
+                static_cast<const uint16_t *>(v), ws.k_pre, ws.v_pre, out, nexus_mass, ws.lse};
+  const float scale_log2 = static_cast<float>(softmax_scale * kLog2e);
+  e = launch_prefill(d, G, grid, stats, rows, ws, Hkv, scale_log2, stream);
+  if (e == hipSuccess && key_weight != nullptr)
+    e = launch_key_weight(batch, total_tokens, Hq, Hkv, d, di->num_cus, cu_seqlens, role,
+                          static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k), ws, scale_log2,
+                          key_weight, dev_status, stream);
   return finish(e, dev_status, stream);
 }
 
@@ -344,12 +366,12 @@ int32_t sonic_nexus_extend(int32_t batch, int32_t total_new, int32_t Hq, int32_t
                          stream);
   if (e != hipSuccess) return SONIC_ERR_HIP;
   if (total_new > 0) {
-    int grid = di->num_cus * di->prefill_blocks[d == 128][G];
+    int grid = di->num_cus * di->prefill_blocks[0][d == 128][G];
     grid = (grid + kNumXcd - 1) / kNumXcd * kNumXcd;
     AttnRows rows{nexus_cu, cache_row_off, static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k),
                   static_cast<const uint16_t *>(v), static_cast<const uint16_t *>(k_cache),
                   static_cast<const uint16_t *>(v_cache), out};
-    e = launch_prefill(d, G, grid, rows, ws, Hkv, static_cast<float>(softmax_scale * kLog2e), stream);
+    e = launch_prefill(d, G, grid, false, rows, ws, Hkv, static_cast<float>(softmax_scale * kLog2e), stream);
     if (e != hipSuccess) return SONIC_ERR_HIP;
   }
   e = launch_extend_append(batch, total_new, Hkv, d, nexus_cu, keep_len, static_cast<uint16_t *>(k_cache),

@@ -80,7 +80,11 @@ struct ReqInfo {
 // Where the rows of an attention call live.  Request b's query rows (and output
 // rows) start at row seg_row0[b] of q/out, its own key rows at row seg_row0[b] of
 // seg_k/seg_v, and its prefix rows at row pre_row0[b] of pre_k/pre_v (row
-// seg_row0[b] when pre_row0 is null).  Rows are [H, D] records.
+// seg_row0[b] when pre_row0 is null).  Rows are [H, D] records.  The statistics
+// outputs, [rows][Hq] like out without D, are written by the statistics variant
+// of the prefill kernel only: the attention mass on prefix keys past the
+// request's system rows (its Nexus keys) and the row's log2-domain softmax
+// normaliser.
 struct AttnRows {
   const int32_t *seg_row0;
   const int64_t *pre_row0;
@@ -90,6 +94,8 @@ struct AttnRows {
   const uint16_t *pre_k;
   const uint16_t *pre_v;
   float *out;
+  float *nexus_mass;
+  float *lse;
 };
 
 // Device workspace of the prefill, carved from one caller buffer.
@@ -103,7 +109,13 @@ struct PrefillWs {
                        //      decreasing tile cost
   uint16_t *k_pre;     // [T, Hkv, D] prefix copies of K and V, request b's rows at offset cu[b]
   uint16_t *v_pre;
-  int32_t *ctrl;       // [16] ctrl[0] = number of descriptors, ctrl[8 + x] = queue head of XCD x
+  int32_t *ctrl;       // [16] ctrl[0] = number of descriptors, ctrl[1] = number of key blocks of
+                       //      the key-weight pass, ctrl[8 + x] = queue head of XCD x
+  // attention statistics (used only when they are asked for)
+  float *lse;          // [T, Hq] log2-domain softmax normaliser of every row and q-head
+  float *wpart;        // [Hkv, T] key weight of every kept key, one partial per kv-head
+  int2 *kblocks;       // [T / 64 + B] (request, block of 64 kept keys) of the key-weight pass
+  int32_t *ncur;       // [B] current-query rows of request b
 };
 
 }  // namespace sonic

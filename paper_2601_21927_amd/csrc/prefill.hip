@@ -131,7 +131,10 @@ __device__ __forceinline__ void stage_tensor(uint16_t *lds_buf, const char *pre_
   }
 }
 
-template <int D, int G>
+// STATS: also write, per row and q-head, the attention mass on the request's
+// Nexus keys (prefix keys at or past its system rows) and the log2-domain softmax
+// normaliser, for the key-weight pass.
+template <int D, int G, bool STATS>
 __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, PrefillWs ws, int Hkv,
                                                                float scale_log2) {
   const uint16_t *__restrict__ q = rows.q;
@@ -216,6 +219,9 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, Pr
     for (int i = 0; i < DB; ++i) oacc[i] = f32x16{};
     float m_run = -INFINITY;   // running max in the log2 domain (lags by at most kLazy)
     float l_run = 0.f;
+    float l_nex = 0.f;         // STATS: the part of l_run from Nexus keys
+    // STATS: Nexus keys are the virtual keys [nex_lo, npre) (the prefix past the system rows)
+    const int nex_lo = STATS ? min(ws.req[t.req].system, npre) : npre;
 
     const int nchunks = (nv + kKeyChunk - 1) / kKeyChunk;
     // One 64-key step: compute on (kc_lds, vc_lds) while step c + 1 streams into
@@ -277,10 +283,15 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, Pr
         const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
         m_run = m_new;
         l_run *= corr;
+        if (STATS) l_nex *= corr;
 #pragma unroll
         for (int db = 0; db < DB; ++db) oacc[db] *= corr;
       }
-      float lsum = 0.f;
+      // STATS: this step's Nexus keys are step-local keys [nx0, nx1)
+      const int nx0 = max(nex_lo - vk0, 0), nx1 = min(npre - vk0, kKeyChunk);
+      const bool nex_all = STATS && nx0 == 0 && nx1 == kKeyChunk;
+      const bool nex_some = STATS && nx0 < nx1 && !nex_all;
+      float lsum = 0.f, nsum = 0.f;
       bf16x8 pb[4];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
@@ -290,11 +301,17 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, Pr
           lo[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][e], scale_log2, -m_run));
           hi[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][8 + e], scale_log2, -m_run));
           lsum += lo[e] + hi[e];
+          if (nex_some) {
+            const int klo = kb * 32 + acc_key(e, g), khi = kb * 32 + acc_key(8 + e, g);
+            nsum += ((klo >= nx0 && klo < nx1) ? lo[e] : 0.f) + ((khi >= nx0 && khi < nx1) ? hi[e] : 0.f);
+          }
         }
         pb[2 * kb] = __builtin_convertvector(lo, bf16x8);
         pb[2 * kb + 1] = __builtin_convertvector(hi, bf16x8);
       }
       l_run += lsum;
+      if (nex_all) l_nex += lsum;
+      if (nex_some) l_nex += nsum;
 
       // ---- O^T += V^T . P^T, V^T operands read transposed from row-major V ----
 #pragma unroll
@@ -331,6 +348,14 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, Pr
     // ---- normalise and store: lane (n, g) holds d = 32*db + 8*i + 4*g + (0..3) ----
     const float l_tot = l_run + __shfl_xor(l_run, 32);
     const float inv = 1.f / l_tot;
+    if (STATS) {
+      const float n_tot = l_nex + __shfl_xor(l_nex, 32);
+      if (n < t.nrows && g == 0) {
+        const size_t idx = static_cast<size_t>(base + t.p0 + n) * Hq + h;
+        if (rows.nexus_mass != nullptr) rows.nexus_mass[idx] = n_tot * inv;
+        rows.lse[idx] = m_run + __builtin_amdgcn_logf(l_tot);
+      }
+    }
     if (n < t.nrows) {
       float *orow = out + (static_cast<size_t>(base + t.p0 + n) * Hq + h) * D;
 #pragma unroll
@@ -347,15 +372,19 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, Pr
 }
 
 template <int D, int G>
-static hipError_t launch_prefill_dg(int grid, AttnRows rows, PrefillWs ws, int Hkv, float scale_log2,
+static hipError_t launch_prefill_dg(int grid, bool stats, AttnRows rows, PrefillWs ws, int Hkv, float scale_log2,
                                     hipStream_t stream) {
-  prefill_kernel<D, G><<<dim3(grid), dim3(G * kWave), 0, stream>>>(rows, ws, Hkv, scale_log2);
+  if (stats)
+    prefill_kernel<D, G, true><<<dim3(grid), dim3(G * kWave), 0, stream>>>(rows, ws, Hkv, scale_log2);
+  else
+    prefill_kernel<D, G, false><<<dim3(grid), dim3(G * kWave), 0, stream>>>(rows, ws, Hkv, scale_log2);
   return hipGetLastError();
 }
 
 template <int D, int G>
-static hipError_t occupancy_dg(int *blocks) {
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, prefill_kernel<D, G>, G * kWave, 0);
+static hipError_t occupancy_dg(bool stats, int *blocks) {
+  if (stats) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, prefill_kernel<D, G, true>, G * kWave, 0);
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, prefill_kernel<D, G, false>, G * kWave, 0);
 }
 
 #define SONIC_FOR_G(D, X) \
@@ -371,8 +400,8 @@ static hipError_t occupancy_dg(int *blocks) {
     default: return hipErrorInvalidValue; \
   }
 
-hipError_t prefill_occupancy(int D, int G, int *blocks) {
-#define OCC(DD, GG) return occupancy_dg<DD, GG>(blocks)
+hipError_t prefill_occupancy(int D, int G, bool stats, int *blocks) {
+#define OCC(DD, GG) return occupancy_dg<DD, GG>(stats, blocks)
   if (D == 64) {
     SONIC_FOR_G(64, OCC)
   } else if (D == 128) {
@@ -382,9 +411,9 @@ hipError_t prefill_occupancy(int D, int G, int *blocks) {
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_prefill(int D, int G, int grid, AttnRows rows, PrefillWs ws, int Hkv, float scale_log2,
-                          hipStream_t stream) {
-#define LAUNCH(DD, GG) return launch_prefill_dg<DD, GG>(grid, rows, ws, Hkv, scale_log2, stream)
+hipError_t launch_prefill(int D, int G, int grid, bool stats, AttnRows rows, PrefillWs ws, int Hkv,
+                          float scale_log2, hipStream_t stream) {
+#define LAUNCH(DD, GG) return launch_prefill_dg<DD, GG>(grid, stats, rows, ws, Hkv, scale_log2, stream)
   if (D == 64) {
     SONIC_FOR_G(64, LAUNCH)
   } else if (D == 128) {

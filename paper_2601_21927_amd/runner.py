@@ -55,14 +55,15 @@ class SonicBatch:
         self.Hq = 0 if self.q is None else self.q.shape[1]
         self.out = None if self.q is None else torch.empty((self.T, self.Hq, self.d), dtype=torch.float32,
                                                            device=self.device)
-        ws = sonic.prefill_workspace_bytes(self.batch, self.total_tokens, self.Hkv, self.d)
+        ws = sonic.prefill_workspace_bytes(self.batch, self.total_tokens, max(self.Hq, 1), self.Hkv, self.d)
         self.prefill_ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=self.device)
         self.cache = None
 
     # ------------------------------------------------------------- step 1
-    def prefill(self, stream=None, nexus_scope: int = sonic.NEXUS_ALL) -> int:
+    def prefill(self, stream=None, nexus_scope: int = sonic.NEXUS_ALL, nexus_mass=None, key_weight=None) -> int:
         return sonic.segment_attn_prefill(self.cu, self.role, self.turn_id, self.q, self.k, self.v, self.out,
-                                          self.prefill_ws, self.status, nexus_scope=nexus_scope, stream=stream)
+                                          self.prefill_ws, self.status, nexus_scope=nexus_scope,
+                                          nexus_mass=nexus_mass, key_weight=key_weight, stream=stream)
 
     # ------------------------------------------------------------- step 2
     def alloc_cache(self, capacities: Sequence[int], fill_bits: int = 0xFFFF):

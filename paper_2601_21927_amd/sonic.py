@@ -63,10 +63,10 @@ def lib() -> ctypes.CDLL:
     L.sonic_layout_stats_host.restype = _i32
     L.sonic_layout_stats_host.argtypes = [_i32, _p, _p, _p, _i32, _p, _p]
     L.sonic_prefill_workspace_bytes.restype = _sz
-    L.sonic_prefill_workspace_bytes.argtypes = [_i32, _i32, _i32, _i32]
+    L.sonic_prefill_workspace_bytes.argtypes = [_i32, _i32, _i32, _i32, _i32]
     L.sonic_segment_attn_prefill.restype = _i32
     L.sonic_segment_attn_prefill.argtypes = [_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _f32, _i32, _p,
-                                             _p, _sz, _p, _p]
+                                             _p, _p, _p, _sz, _p, _p]
     L.sonic_kv_compact.restype = _i32
     L.sonic_kv_compact.argtypes = [_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p]
     L.sonic_decode_workspace_bytes.restype = _sz
@@ -153,24 +153,26 @@ def layout_stats_host(cu_seqlens, role, turn_id, nexus_scope: int = NEXUS_ALL):
 
 
 # ----------------------------------------------------------------- step 1: prefill
-def prefill_workspace_bytes(batch: int, total_tokens: int, num_kv_heads: int, head_dim: int) -> int:
-    return int(lib().sonic_prefill_workspace_bytes(batch, total_tokens, num_kv_heads, head_dim))
+def prefill_workspace_bytes(batch: int, total_tokens: int, num_q_heads: int, num_kv_heads: int, head_dim: int) -> int:
+    return int(lib().sonic_prefill_workspace_bytes(batch, total_tokens, num_q_heads, num_kv_heads, head_dim))
 
 
 def segment_attn_prefill(cu_seqlens, role, turn_id, q, k, v, out, workspace, dev_status, softmax_scale=None,
-                         nexus_scope: int = NEXUS_ALL, stream=None) -> int:
+                         nexus_scope: int = NEXUS_ALL, nexus_mass=None, key_weight=None, stream=None) -> int:
     """q [T,Hq,d] bf16, k/v [T,Hkv,d] bf16, out [T,Hq,d] fp32; cu int32 [B+1]; role uint8 [T];
-    turn_id int32 [T]; workspace uint8 [>= prefill_workspace_bytes]; dev_status int32 [1]."""
-    _dev(cu_seqlens, role, turn_id, q, k, v, out, workspace, dev_status)
+    turn_id int32 [T]; workspace uint8 [>= prefill_workspace_bytes]; dev_status int32 [1];
+    optional statistics nexus_mass fp32 [T,Hq] and key_weight fp32 [T]."""
+    _dev(cu_seqlens, role, turn_id, q, k, v, out, workspace, dev_status, nexus_mass, key_weight)
     _types(cu_seqlens=(cu_seqlens, _I32), role=(role, _U8), turn_id=(turn_id, _I32), q=(q, _BF16), k=(k, _BF16),
-           v=(v, _BF16), out=(out, _F32), dev_status=(dev_status, _I32))
+           v=(v, _BF16), out=(out, _F32), dev_status=(dev_status, _I32), nexus_mass=(nexus_mass, _F32),
+           key_weight=(key_weight, _F32))
     T, Hq, d = q.shape
     Hkv = k.shape[1]
     scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
     return int(lib().sonic_segment_attn_prefill(
         cu_seqlens.numel() - 1, T, Hq, Hkv, d, _ptr(cu_seqlens), _ptr(role), _ptr(turn_id), _ptr(q), _ptr(k),
-        _ptr(v), scale, int(nexus_scope), _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(),
-        _ptr(dev_status), _stream(stream)))
+        _ptr(v), scale, int(nexus_scope), _ptr(out), _ptr(nexus_mass), _ptr(key_weight), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(dev_status), _stream(stream)))
 
 
 # ----------------------------------------------------------------- step 2: compaction

@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert sonic.abi_version() == 4
+    assert sonic.abi_version() == 5
     assert sonic.status_string(0) == "ok"
     for code in range(1, 7):
         assert sonic.status_string(code) != "unknown status"
@@ -126,7 +126,9 @@ def test_layout_stats_on_workloads(idx, pairs):
 
 def test_workspace_sizes():
     # plan (44 B per token) plus the prefix copies of K and V (Hkv * d * 4 B per token)
-    assert sonic.prefill_workspace_bytes(8, 43392, 8, 128) >= 43392 * (44 + 8 * 128 * 4)
-    assert sonic.prefill_workspace_bytes(0, 0, 1, 64) > 0
-    assert sonic.prefill_workspace_bytes(1, 10, 0, 64) == 0
+    # plan (44 B per token), K/V prefix copies, softmax normalisers and key-weight partials
+    assert sonic.prefill_workspace_bytes(8, 43392, 32, 8, 128) >= 43392 * (44 + 8 * 128 * 4 + (32 + 8) * 4)
+    assert sonic.prefill_workspace_bytes(0, 0, 1, 1, 64) > 0
+    assert sonic.prefill_workspace_bytes(1, 10, 4, 0, 64) == 0
+    assert sonic.prefill_workspace_bytes(1, 10, 0, 2, 64) == 0
     assert sonic.decode_workspace_bytes(8, 32, 128, 1584) >= 8 * 32 * 130 * 4
