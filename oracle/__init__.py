@@ -28,9 +28,12 @@ those definitions out, slowly and in float64:
                    Sec. 4: the Nexus attention mass per query row and head, and
                    the head-averaged attention each key receives from the
                    current rows.
+* ``projection`` - the role-routed linear layer: Nexus tokens use their own
+                   projection matrices, every other token the standard ones
+                   (Sec. 3.1).
 
 Inputs are bf16 bit patterns (uint16); they are widened exactly to float64.
 """
-from . import layout, mask, attention, compaction, decode, extend, stats  # noqa: F401
+from . import layout, mask, attention, compaction, decode, extend, stats, projection  # noqa: F401
 
 
