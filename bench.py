@@ -293,6 +293,27 @@ def main():
     assert np.array_equal(ext_len.cpu().numpy(), ext_keep_np + kn_np)
     ext_flops = float(4 * d * Hq * np.sum(kn_np * (ext_len_np + kn_np)))
 
+    # ---- role-routed projection: the fused QKV product of the 8B shape over the whole batch,
+    # Nexus rows with their own weight set (K = 4096 model width, N = 4096 + 2 x 1024) ----
+    pj_K, pj_N = 4096, Hq * d + 2 * Hkv * d
+    gen = torch.Generator(device=dev).manual_seed(11)
+    pj_x = torch.randn((batch.total_tokens, pj_K), generator=gen, device=dev).to(torch.bfloat16)
+    pj_wt = (torch.randn((pj_N, pj_K), generator=gen, device=dev) * 0.02).to(torch.bfloat16)
+    pj_wn = (torch.randn((pj_N, pj_K), generator=gen, device=dev) * 0.02).to(torch.bfloat16)
+    pj_y = torch.empty((batch.total_tokens, pj_N), dtype=torch.float32, device=dev)
+    pj_ws = torch.empty(sonic.role_projection_workspace_bytes(batch.total_tokens), dtype=torch.uint8, device=dev)
+
+    def run_projection():
+        st = sonic.role_projection(db.role, pj_x, pj_wt, pj_wn, pj_y, pj_ws, db.status)
+        assert st == sonic.OK, sonic.status_string(st)
+    phases["projection"] = run_projection
+    run_projection()
+    torch.cuda.synchronize()
+    pj_ms = back_to_back("projection", 5)
+    pj_flops = 2.0 * batch.total_tokens * pj_K * pj_N
+    assert db.read_status() == 0
+    del pj_x, pj_y
+
     # ---- algorithmic work ----
     row_bytes = Hkv * d * 2                       # one token's K (or V) over all kv-heads, bf16
     compact_bytes = float(kept.sum()) * row_bytes * 2 * 2 + batch.total_tokens + float(kept.sum()) * 4
@@ -350,10 +371,15 @@ def main():
             "next_turn_nexus_us": round(ext_ms * 1e3, 2),
             "next_turn_nexus_tflops": round(ext_flops / (ext_ms * 1e-3) / 1e12, 2),
             "next_turn_nexus_frac_bf16_peak": round(ext_flops / (ext_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "role_projection_qkv_ms": round(pj_ms, 4),
+            "role_projection_qkv_tflops": round(pj_flops / (pj_ms * 1e-3) / 1e12, 2),
+            "role_projection_qkv_frac_bf16_peak": round(pj_flops / (pj_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         },
         "work": {"visible_flops": visible_flops, "compact_bytes": compact_bytes, "decode_bytes": decode_bytes,
                  "full_decode_bytes": full_bytes, "next_turn_nexus_flops": ext_flops,
-                 "next_turn_nexus": f"{len(allpos)} new Nexus rows over caches of {int(ext_len_np.max())} rows"},
+                 "next_turn_nexus": f"{len(allpos)} new Nexus rows over caches of {int(ext_len_np.max())} rows",
+                 "role_projection_qkv_flops": pj_flops,
+                 "role_projection_qkv": f"T={batch.total_tokens} K={pj_K} N={pj_N}, fp32 out"},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

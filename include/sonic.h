@@ -92,7 +92,7 @@ enum {
     SONIC_NEXUS_UP_TO_OWN = 1
 };
 
-/* Version of this ABI (bumped on any signature or layout change). */
+/* Version of this ABI (bumped on any signature or layout change or addition). */
 int32_t sonic_abi_version(void);
 
 /* Static text for a status code. */
@@ -183,6 +183,35 @@ int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t 
                                    const void *v, float softmax_scale, int32_t nexus_scope, float *out,
                                    float *nexus_mass, float *key_weight, void *workspace, size_t workspace_bytes,
                                    int32_t *dev_status, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Role-routed linear layer (the projections around the attention)          */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of device workspace sonic_role_projection needs (0 for T < 0). */
+size_t sonic_role_projection_workspace_bytes(int32_t total_tokens);
+
+/*
+ * y[t] = W_N x[t] for every Nexus row t, y[t] = W x[t] for every other row
+ * (system, history text, current, generated): Nexus tokens have their own
+ * projection matrices and MLP branches (Sec. 3.1), so every linear layer of
+ * the block is this routed product with that layer's two weight sets.
+ *
+ *   total_tokens    T (host value), any T >= 0
+ *   in_features     K, a positive multiple of 64
+ *   out_features    N >= 1
+ *   role            device uint8 [T] (SONIC_ROLE_*); rows are routed by it alone
+ *   x               device bf16 [T][K]
+ *   w_text, w_nexus device bf16 [N][K] each (output-by-input, as a linear layer stores it)
+ *   y               device fp32 [T][N], every row written
+ *   workspace       device, >= sonic_role_projection_workspace_bytes(T), 256-byte aligned
+ *   dev_status      device int32; while it is non-zero nothing is written
+ * Products are accumulated in fp32 from exact bf16 products.
+ */
+int32_t sonic_role_projection(int32_t total_tokens, int32_t in_features, int32_t out_features,
+                              const uint8_t *role, const void *x, const void *w_text, const void *w_nexus,
+                              float *y, void *workspace, size_t workspace_bytes, int32_t *dev_status,
+                              void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Step 2: KV compaction                                                     */

@@ -13,6 +13,9 @@ hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus,
                        const uint8_t *role, const int32_t *turn, const uint16_t *k, const uint16_t *v, PrefillWs ws,
                        int32_t *status, hipStream_t stream);
 hipError_t prefill_occupancy(int D, int G, bool stats, int *blocks);
+hipError_t launch_routed_gemm(int T, int K, int N, const uint8_t *role, const uint16_t *x, const uint16_t *w_text,
+                              const uint16_t *w_nexus, float *y, int32_t *blk_nexus, int32_t *counts, int32_t *perm,
+                              int32_t *status, hipStream_t stream);
 hipError_t launch_key_weight(int batch, int T, int Hq, int Hkv, int D, int num_cus, const int32_t *cu,
                              const uint8_t *role, const uint16_t *q, const uint16_t *k, PrefillWs ws,
                              float scale_log2, float *w, int32_t *status, hipStream_t stream);
@@ -38,7 +41,7 @@ hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int nsp
 
 namespace {
 
-constexpr int kAbiVersion = 5;
+constexpr int kAbiVersion = 6;
 constexpr double kLog2e = 1.4426950408889634;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -377,6 +380,47 @@ int32_t sonic_nexus_extend(int32_t batch, int32_t total_new, int32_t Hq, int32_t
   e = launch_extend_append(batch, total_new, Hkv, d, nexus_cu, keep_len, static_cast<uint16_t *>(k_cache),
                            static_cast<uint16_t *>(v_cache), cache_row_off, cache_len,
                            static_cast<const uint16_t *>(k), static_cast<const uint16_t *>(v), dev_status, stream);
+  return finish(e, dev_status, stream);
+}
+
+// ---------------------------------------------------------------- role-routed projection
+static size_t projection_ws_layout(int32_t T, char *base, int32_t **blk, int32_t **counts, int32_t **perm) {
+  const size_t T1 = static_cast<size_t>(T > 0 ? T : 1);
+  const size_t nblk = (T1 + 1023) / 1024;
+  const size_t b_bytes = align_up(nblk * sizeof(int32_t), 256);
+  const size_t c_bytes = 256;
+  const size_t p_bytes = align_up(T1 * sizeof(int32_t), 256);
+  if (base) {
+    *blk = reinterpret_cast<int32_t *>(base);
+    *counts = reinterpret_cast<int32_t *>(base + b_bytes);
+    *perm = reinterpret_cast<int32_t *>(base + b_bytes + c_bytes);
+  }
+  return b_bytes + c_bytes + p_bytes;
+}
+
+size_t sonic_role_projection_workspace_bytes(int32_t total_tokens) {
+  if (total_tokens < 0) return 0;
+  return projection_ws_layout(total_tokens, nullptr, nullptr, nullptr, nullptr);
+}
+
+int32_t sonic_role_projection(int32_t T, int32_t K, int32_t N, const uint8_t *role, const void *x,
+                              const void *w_text, const void *w_nexus, float *y, void *workspace,
+                              size_t workspace_bytes, int32_t *dev_status, void *stream_) {
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  if (T < 0 || K <= 0 || N <= 0 || dev_status == nullptr) return SONIC_ERR_INVALID_ARG;
+  if (K % 64 != 0) return SONIC_ERR_UNSUPPORTED;
+  if (T == 0) return SONIC_OK;
+  if (!role || !x || !w_text || !w_nexus || !y || !workspace) return SONIC_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(w_text, 16) || !aligned(w_nexus, 16) || !aligned(y, 4) ||
+      !aligned(workspace, 256))
+    return SONIC_ERR_INVALID_ARG;
+  int32_t *blk = nullptr, *counts = nullptr, *perm = nullptr;
+  if (workspace_bytes < projection_ws_layout(T, static_cast<char *>(workspace), &blk, &counts, &perm))
+    return SONIC_ERR_WORKSPACE;
+  const hipError_t e = launch_routed_gemm(T, K, N, role, static_cast<const uint16_t *>(x),
+                                          static_cast<const uint16_t *>(w_text),
+                                          static_cast<const uint16_t *>(w_nexus), y, blk, counts, perm, dev_status,
+                                          stream);
   return finish(e, dev_status, stream);
 }
 

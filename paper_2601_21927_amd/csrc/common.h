@@ -35,6 +35,40 @@ __device__ __forceinline__ bool block_status_clear(const int32_t *status, int *l
   return *lds_flag != 0;
 }
 
+// s_waitcnt vmcnt(N), the other counters left at their maximum (gfx9 encoding):
+// wait until at most N of this wave's vector-memory operations are outstanding.
+// They complete in issue order, so this waits for all but the N most recent.
+template <int N> __device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier for the LDS pipeline.  __syncthreads() would also wait for
+// every outstanding vector-memory operation (its release fence covers the
+// direct-to-LDS loads still in flight), which would drain the prefetch; here the
+// loads a step needs are waited for explicitly with wait_vm, this wave's LDS
+// reads are completed (lgkmcnt(0)) before it arrives, and the signal fences keep
+// the compiler from moving memory operations across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));   // lgkmcnt(0)
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// One direct-to-LDS load: every lane fetches 16 bytes from its global address
+// and the wave writes them to LDS at dst + 16 * lane (dst is wave-uniform, passed
+// in M0).  Written as inline assembly so that the compiler does not track it as a
+// pending LDS write: it would otherwise wait for every such load, including the
+// prefetches into the other buffers, before each LDS read.  Completion is waited
+// for explicitly (wait_vm) before the data is read.
+__device__ __forceinline__ void dma_row16(const char *src, const uint16_t *dst) {
+  // C-style cast: converting the LDS pointer to its 32-bit address
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
+      reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) uint16_t *)dst)));
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds) : "memory", "m0");
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 

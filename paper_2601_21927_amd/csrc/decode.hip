@@ -71,11 +71,6 @@ __device__ __forceinline__ int atomic_inc_pending(int32_t *p) {
   asm volatile("global_atomic_add %0, %1, %2, off sc0" : "=v"(old) : "v"(p), "v"(1) : "memory");
   return old;
 }
-// s_waitcnt vmcnt(N), other counters at their maximum (gfx9 encoding)
-template <int N> __device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
 
 template <int D, int G, bool MASKED>
 __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(

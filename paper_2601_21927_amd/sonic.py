@@ -32,7 +32,7 @@ EXPORTS = (
     "sonic_abi_version", "sonic_status_string", "sonic_validate_layout_host", "sonic_layout_stats_host",
     "sonic_prefill_workspace_bytes", "sonic_segment_attn_prefill", "sonic_kv_compact",
     "sonic_decode_workspace_bytes", "sonic_compressed_decode", "sonic_nexus_extend_workspace_bytes",
-    "sonic_nexus_extend",
+    "sonic_nexus_extend", "sonic_role_projection_workspace_bytes", "sonic_role_projection",
 )
 
 _lib = None
@@ -79,6 +79,10 @@ def lib() -> ctypes.CDLL:
     L.sonic_nexus_extend.restype = _i32
     L.sonic_nexus_extend.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p,
                                      _f32, _p, _p, _sz, _p, _p]
+    L.sonic_role_projection_workspace_bytes.restype = _sz
+    L.sonic_role_projection_workspace_bytes.argtypes = [_i32]
+    L.sonic_role_projection.restype = _i32
+    L.sonic_role_projection.argtypes = [_i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _sz, _p, _p]
     _lib = L
     return L
 
@@ -234,3 +238,23 @@ def nexus_extend(nexus_cu, keep_len, k_cache, v_cache, cache_row_off, cache_row_
         _ptr(v_cache), _ptr(cache_row_off), _ptr(cache_row_cap), _ptr(cache_len), _ptr(q), _ptr(k), _ptr(v), scale,
         _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(dev_status),
         _stream(stream)))
+
+
+# ----------------------------------------------------------------- role-routed projection
+def role_projection_workspace_bytes(total_tokens: int) -> int:
+    return int(lib().sonic_role_projection_workspace_bytes(total_tokens))
+
+
+def role_projection(role, x, w_text, w_nexus, y, workspace, dev_status, stream=None) -> int:
+    """role uint8 [T]; x [T,K] bf16; w_text / w_nexus [N,K] bf16; y [T,N] fp32 (Nexus rows use w_nexus)."""
+    _dev(role, x, w_text, w_nexus, y, workspace, dev_status)
+    _types(role=(role, _U8), x=(x, _BF16), w_text=(w_text, _BF16), w_nexus=(w_nexus, _BF16), y=(y, _F32),
+           dev_status=(dev_status, _I32))
+    T, K = x.shape
+    N = w_text.shape[0]
+    if tuple(w_nexus.shape) != (N, K) or tuple(w_text.shape) != (N, K) or tuple(y.shape) != (T, N) or \
+            role.numel() != T:
+        raise ValueError("role_projection: inconsistent shapes")
+    return int(lib().sonic_role_projection(
+        T, K, N, _ptr(role), _ptr(x), _ptr(w_text), _ptr(w_nexus), _ptr(y), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(dev_status), _stream(stream)))
