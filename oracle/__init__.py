@@ -31,9 +31,13 @@ those definitions out, slowly and in float64:
 * ``projection`` - the role-routed linear layer: Nexus tokens use their own
                    projection matrices, every other token the standard ones
                    (Sec. 3.1).
+* ``recon``      - the reconstruction targets of the information bottleneck
+                   (Sec. 4): per Nexus token, a cosine-softmax pooling of its
+                   body sub-interval, with the target's cosine and the
+                   normalised entropy of the weights.
 
 Inputs are bf16 bit patterns (uint16); they are widened exactly to float64.
 """
-from . import layout, mask, attention, compaction, decode, extend, stats, projection  # noqa: F401
+from . import layout, mask, attention, compaction, decode, extend, stats, projection, recon  # noqa: F401
 
 
