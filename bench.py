@@ -314,6 +314,27 @@ def main():
     assert db.read_status() == 0
     del pj_x, pj_y
 
+    # ---- reconstruction targets of the whole batch, hidden size 4096 (training side) ----
+    rc_Dm = 4096
+    rc_h = torch.randn((batch.total_tokens, rc_Dm), generator=gen, device=dev).to(torch.bfloat16)
+    rc_n = int((batch.role == W.ROLE_NEXUS).sum())
+    rc_t = torch.empty((rc_n, rc_Dm), dtype=torch.float32, device=dev)
+    rc_c = torch.empty((rc_n,), dtype=torch.float32, device=dev)
+    rc_r = torch.empty((rc_n,), dtype=torch.float32, device=dev)
+    rc_ws = torch.empty(sonic.nexus_recon_workspace_bytes(B, batch.total_tokens), dtype=torch.uint8, device=dev)
+
+    def run_recon():
+        st = sonic.nexus_recon_targets(db.cu, db.role, db.turn_id, rc_h, rc_t, rc_c, rc_r, rc_ws, db.status)
+        assert st == sonic.OK, sonic.status_string(st)
+    phases["recon"] = run_recon
+    run_recon()
+    torch.cuda.synchronize()
+    rc_ms = back_to_back("recon", 10)
+    assert db.read_status() == 0
+    body_rows = sum(sum(l.bodies[i] for i in range(len(l.bodies)) if l.nexus[i] > 0) for l in batch.layouts)
+    rc_bytes = float(body_rows + rc_n) * rc_Dm * 2 + rc_n * (rc_Dm * 4 + 8)
+    del rc_h
+
     # ---- algorithmic work ----
     row_bytes = Hkv * d * 2                       # one token's K (or V) over all kv-heads, bf16
     compact_bytes = float(kept.sum()) * row_bytes * 2 * 2 + batch.total_tokens + float(kept.sum()) * 4
@@ -374,12 +395,17 @@ def main():
             "role_projection_qkv_ms": round(pj_ms, 4),
             "role_projection_qkv_tflops": round(pj_flops / (pj_ms * 1e-3) / 1e12, 2),
             "role_projection_qkv_frac_bf16_peak": round(pj_flops / (pj_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "recon_targets_us": round(rc_ms * 1e3, 2),
+            "recon_targets_gbs": round(rc_bytes / (rc_ms * 1e-3) / 1e9, 1),
+            "recon_targets_frac_hbm_peak": round(rc_bytes / (rc_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
         },
         "work": {"visible_flops": visible_flops, "compact_bytes": compact_bytes, "decode_bytes": decode_bytes,
                  "full_decode_bytes": full_bytes, "next_turn_nexus_flops": ext_flops,
                  "next_turn_nexus": f"{len(allpos)} new Nexus rows over caches of {int(ext_len_np.max())} rows",
                  "role_projection_qkv_flops": pj_flops,
-                 "role_projection_qkv": f"T={batch.total_tokens} K={pj_K} N={pj_N}, fp32 out"},
+                 "role_projection_qkv": f"T={batch.total_tokens} K={pj_K} N={pj_N}, fp32 out",
+                 "recon_targets_bytes": rc_bytes,
+                 "recon_targets": f"{rc_n} Nexus tokens, hidden size {rc_Dm}"},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

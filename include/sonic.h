@@ -214,6 +214,43 @@ int32_t sonic_role_projection(int32_t total_tokens, int32_t in_features, int32_t
                               void *stream);
 
 /* ------------------------------------------------------------------------ */
+/* Reconstruction targets of the Nexus tokens (training side)                */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of device workspace sonic_nexus_recon_targets needs (0 for negative sizes). */
+size_t sonic_nexus_recon_workspace_bytes(int32_t batch, int32_t total_tokens);
+
+/*
+ * Per Nexus token, the reconstruction target of the information bottleneck
+ * (Sec. 4): the body of its history segment is cut into one sub-interval per
+ * Nexus token of the segment, interval j of a b-token body for K Nexus tokens
+ * being [floor(j b / K), max(floor((j + 1) b / K), floor(j b / K) + 1)) (near-
+ * equal pieces; single tokens when b < K), and
+ *     target_j = sum over x of alpha(x) h(x),  alpha = softmax over x of cos(h(N_j), h(x)).
+ * A zero vector has cosine 0 with anything.
+ *
+ *   batch, total_tokens   B, T (host values)
+ *   hidden                hidden size Dm: a positive multiple of 8, at most 16384
+ *   cu_seqlens, role, turn_id   device, the layout as for the prefill
+ *   h                     device bf16 [T][Dm]: the hidden states
+ *   max_rows              rows of the three outputs (>= the batch's Nexus count)
+ *   target                device fp32 [n][Dm]: one row per Nexus token of the batch,
+ *                         in packed position order
+ *   cos_target            device fp32 [n]: cos(h(N_j), target_j)
+ *   entropy_ratio         device fp32 [n]: H(alpha) / log |interval| (1 for one token)
+ *   workspace             device, >= sonic_nexus_recon_workspace_bytes(B, T), 256-byte aligned
+ *   dev_status            device int32: SONIC_ERR_BAD_LAYOUT for a grammar error,
+ *                         SONIC_ERR_CAPACITY when the Nexus count exceeds max_rows;
+ *                         then nothing is written
+ * Reproducible: the reductions run in a fixed order.
+ */
+int32_t sonic_nexus_recon_targets(int32_t batch, int32_t total_tokens, int32_t hidden,
+                                  const int32_t *cu_seqlens, const uint8_t *role, const int32_t *turn_id,
+                                  const void *h, int32_t max_rows, float *target, float *cos_target,
+                                  float *entropy_ratio, void *workspace, size_t workspace_bytes,
+                                  int32_t *dev_status, void *stream);
+
+/* ------------------------------------------------------------------------ */
 /* Step 2: KV compaction                                                     */
 /* ------------------------------------------------------------------------ */
 

@@ -13,6 +13,10 @@ hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus,
                        const uint8_t *role, const int32_t *turn, const uint16_t *k, const uint16_t *v, PrefillWs ws,
                        int32_t *status, hipStream_t stream);
 hipError_t prefill_occupancy(int D, int G, bool stats, int *blocks);
+hipError_t launch_recon(int batch, int total_tokens, int Dm, int max_rows, int num_cus, const int32_t *cu,
+                        const uint8_t *role, const int32_t *turn, const uint16_t *h, PrefillWs ws,
+                        int32_t *nexus_off, int4 *items, float *target, float *cos_out, float *ratio_out,
+                        int32_t *status, hipStream_t stream);
 hipError_t launch_routed_gemm(int T, int K, int N, const uint8_t *role, const uint16_t *x, const uint16_t *w_text,
                               const uint16_t *w_nexus, float *y, int32_t *blk_nexus, int32_t *counts, int32_t *perm,
                               int32_t *status, hipStream_t stream);
@@ -41,7 +45,7 @@ hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int nsp
 
 namespace {
 
-constexpr int kAbiVersion = 6;
+constexpr int kAbiVersion = 7;
 constexpr double kLog2e = 1.4426950408889634;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -421,6 +425,68 @@ int32_t sonic_role_projection(int32_t T, int32_t K, int32_t N, const uint8_t *ro
                                           static_cast<const uint16_t *>(w_text),
                                           static_cast<const uint16_t *>(w_nexus), y, blk, counts, perm, dev_status,
                                           stream);
+  return finish(e, dev_status, stream);
+}
+
+// ---------------------------------------------------------------- reconstruction targets
+static size_t recon_ws_layout(int32_t batch, int32_t T, PrefillWs *ws, int32_t **nexus_off, int4 **items,
+                              char *base) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes, 256);
+    return base ? base + o : nullptr;
+  };
+  const size_t B1 = static_cast<size_t>(batch > 0 ? batch : 1);
+  const size_t T1 = static_cast<size_t>(T > 0 ? T : 1);
+  char *req = take(sizeof(ReqInfo) * B1);
+  char *ppos = take(sizeof(int32_t) * T1);
+  char *runs = take(sizeof(int2) * T1);
+  char *tiles = take(sizeof(TileDesc) * T1);
+  char *ctrl = take(sizeof(int32_t) * 16);
+  char *noff = take(sizeof(int32_t) * B1);
+  char *it = take(sizeof(int4) * T1);
+  if (ws) {
+    *ws = PrefillWs{};
+    ws->req = reinterpret_cast<ReqInfo *>(req);
+    ws->prefix_pos = reinterpret_cast<int32_t *>(ppos);
+    ws->runs = reinterpret_cast<int2 *>(runs);
+    ws->tiles = reinterpret_cast<TileDesc *>(tiles);
+    ws->ctrl = reinterpret_cast<int32_t *>(ctrl);
+    *nexus_off = reinterpret_cast<int32_t *>(noff);
+    *items = reinterpret_cast<int4 *>(it);
+  }
+  return off;
+}
+
+size_t sonic_nexus_recon_workspace_bytes(int32_t batch, int32_t total_tokens) {
+  if (batch < 0 || total_tokens < 0) return 0;
+  return recon_ws_layout(batch, total_tokens, nullptr, nullptr, nullptr, nullptr);
+}
+
+int32_t sonic_nexus_recon_targets(int32_t batch, int32_t T, int32_t Dm, const int32_t *cu_seqlens,
+                                  const uint8_t *role, const int32_t *turn_id, const void *h, int32_t max_rows,
+                                  float *target, float *cos_target, float *entropy_ratio, void *workspace,
+                                  size_t workspace_bytes, int32_t *dev_status, void *stream_) {
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  if (batch < 0 || T < 0 || Dm <= 0 || max_rows < 0 || dev_status == nullptr) return SONIC_ERR_INVALID_ARG;
+  if (Dm % 8 != 0 || Dm > 16384) return SONIC_ERR_UNSUPPORTED;
+  if (batch > 65535) return SONIC_ERR_UNSUPPORTED;
+  if (batch == 0 || T == 0) return SONIC_OK;
+  if (!cu_seqlens || !role || !turn_id || !h || !workspace || (max_rows > 0 && (!target || !cos_target ||
+                                                                                  !entropy_ratio)))
+    return SONIC_ERR_INVALID_ARG;
+  if (!aligned(h, 16) || !aligned(target, 16) || !aligned(workspace, 256)) return SONIC_ERR_INVALID_ARG;
+  PrefillWs ws;
+  int32_t *nexus_off = nullptr;
+  int4 *items = nullptr;
+  if (workspace_bytes < recon_ws_layout(batch, T, &ws, &nexus_off, &items, static_cast<char *>(workspace)))
+    return SONIC_ERR_WORKSPACE;
+  DeviceInfo *di = nullptr;
+  hipError_t e = device_info(&di);
+  if (e != hipSuccess) return SONIC_ERR_HIP;
+  e = launch_recon(batch, T, Dm, max_rows, di->num_cus, cu_seqlens, role, turn_id, static_cast<const uint16_t *>(h),
+                   ws, nexus_off, items, target, cos_target, entropy_ratio, dev_status, stream);
   return finish(e, dev_status, stream);
 }
 

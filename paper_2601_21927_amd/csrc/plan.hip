@@ -291,6 +291,15 @@ hipError_t launch_plan_order(int batch, const int32_t *cu, PrefillWs ws, int32_t
   return hipGetLastError();
 }
 
+// Grammar check and run table only (ws.req, ws.prefix_pos, ws.runs; ws.tiles is
+// written as scratch), for callers that need the segment structure but no prefill.
+hipError_t launch_plan_runs(int batch, int total_tokens, const int32_t *cu, const uint8_t *role, const int32_t *turn,
+                            PrefillWs ws, int32_t *status, hipStream_t stream) {
+  plan_runs_kernel<<<dim3(batch), dim3(kPlanThreads), 0, stream>>>(cu, role, turn, ws, total_tokens,
+                                                                    SONIC_NEXUS_ALL, status);
+  return hipGetLastError();
+}
+
 hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus, int nexus_scope, const int32_t *cu,
                        const uint8_t *role, const int32_t *turn, const uint16_t *k, const uint16_t *v, PrefillWs ws,
                        int32_t *status, hipStream_t stream) {

@@ -33,6 +33,7 @@ EXPORTS = (
     "sonic_prefill_workspace_bytes", "sonic_segment_attn_prefill", "sonic_kv_compact",
     "sonic_decode_workspace_bytes", "sonic_compressed_decode", "sonic_nexus_extend_workspace_bytes",
     "sonic_nexus_extend", "sonic_role_projection_workspace_bytes", "sonic_role_projection",
+    "sonic_nexus_recon_workspace_bytes", "sonic_nexus_recon_targets",
 )
 
 _lib = None
@@ -83,6 +84,10 @@ def lib() -> ctypes.CDLL:
     L.sonic_role_projection_workspace_bytes.argtypes = [_i32]
     L.sonic_role_projection.restype = _i32
     L.sonic_role_projection.argtypes = [_i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _sz, _p, _p]
+    L.sonic_nexus_recon_workspace_bytes.restype = _sz
+    L.sonic_nexus_recon_workspace_bytes.argtypes = [_i32, _i32]
+    L.sonic_nexus_recon_targets.restype = _i32
+    L.sonic_nexus_recon_targets.argtypes = [_i32, _i32, _i32, _p, _p, _p, _p, _i32, _p, _p, _p, _p, _sz, _p, _p]
     _lib = L
     return L
 
@@ -258,3 +263,26 @@ def role_projection(role, x, w_text, w_nexus, y, workspace, dev_status, stream=N
     return int(lib().sonic_role_projection(
         T, K, N, _ptr(role), _ptr(x), _ptr(w_text), _ptr(w_nexus), _ptr(y), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _ptr(dev_status), _stream(stream)))
+
+
+# ----------------------------------------------------------------- reconstruction targets
+def nexus_recon_workspace_bytes(batch: int, total_tokens: int) -> int:
+    return int(lib().sonic_nexus_recon_workspace_bytes(batch, total_tokens))
+
+
+def nexus_recon_targets(cu_seqlens, role, turn_id, h, target, cos_target, entropy_ratio, workspace, dev_status,
+                        stream=None) -> int:
+    """h [T,Dm] bf16; target [n,Dm] fp32, cos_target [n] fp32, entropy_ratio [n] fp32 with n >= the
+    batch's Nexus count (rows in packed position order)."""
+    _dev(cu_seqlens, role, turn_id, h, target, cos_target, entropy_ratio, workspace, dev_status)
+    _types(cu_seqlens=(cu_seqlens, _I32), role=(role, _U8), turn_id=(turn_id, _I32), h=(h, _BF16),
+           target=(target, _F32), cos_target=(cos_target, _F32), entropy_ratio=(entropy_ratio, _F32),
+           dev_status=(dev_status, _I32))
+    T, Dm = h.shape
+    n = target.shape[0]
+    if target.shape[1] != Dm or cos_target.numel() < n or entropy_ratio.numel() < n:
+        raise ValueError("nexus_recon_targets: inconsistent output shapes")
+    return int(lib().sonic_nexus_recon_targets(
+        cu_seqlens.numel() - 1, T, Dm, _ptr(cu_seqlens), _ptr(role), _ptr(turn_id), _ptr(h), n, _ptr(target),
+        _ptr(cos_target), _ptr(entropy_ratio), _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _ptr(dev_status), _stream(stream)))
