@@ -53,29 +53,44 @@ __global__ __launch_bounds__(1024) void recon_offsets_kernel(int batch, int max_
 }
 
 // Per request: one item per Nexus token, (position, first interval row, end row), rows
-// as batch positions.
+// as batch positions.  The run table is read 256 runs at a time into LDS; then the
+// workgroup walks those runs and its threads fill a Nexus run's items in parallel.
 __global__ __launch_bounds__(256) void recon_items_kernel(const int32_t *__restrict__ cu,
                                                           const uint8_t *__restrict__ role, PrefillWs ws,
                                                           const int32_t *__restrict__ nexus_off,
                                                           int4 *__restrict__ items) {
+  __shared__ int s_x[256 + 2];    // starts of runs c0 - 1 .. c0 + 256 (the last: the next run or L)
+  __shared__ int s_y[256];        // prefix rows (system + Nexus) before each run
+  __shared__ int s_nx[256];       // run is a Nexus run
   if (ws.ctrl[0] == 0) return;
   const int b = blockIdx.x;
   const int s0 = cu[b];
   const int L = cu[b + 1] - s0;
   const ReqInfo ri = ws.req[b];
-  for (int r = threadIdx.x; r < ri.nruns; r += 256) {
-    const int start = ws.runs[s0 + r].x;
-    if (role[s0 + start] != kNexus) continue;   // the grammar puts its body run right before
-    const int body = ws.runs[s0 + r - 1].x;
-    const int blen = start - body;
-    const int end = r + 1 < ri.nruns ? ws.runs[s0 + r + 1].x : L;
-    const int K = end - start;
-    const int first = nexus_off[b] + ws.runs[s0 + r].y - ri.system;   // Nexus tokens before this run
-    for (int j = 0; j < K; ++j) {
-      const int s = static_cast<int>(static_cast<int64_t>(j) * blen / K);
-      const int e = max(static_cast<int>(static_cast<int64_t>(j + 1) * blen / K), s + 1);
-      items[first + j] = make_int4(s0 + start + j, s0 + body + s, s0 + body + e, 0);
+  const int base = nexus_off[b] - ri.system;
+  for (int c0 = 0; c0 < ri.nruns; c0 += 256) {
+    const int cnt = min(256, ri.nruns - c0);
+    if (threadIdx.x < cnt) {
+      const int2 run = ws.runs[s0 + c0 + threadIdx.x];
+      s_x[threadIdx.x + 1] = run.x;
+      s_y[threadIdx.x] = run.y;
+      s_nx[threadIdx.x] = role[s0 + run.x] == kNexus;
     }
+    if (threadIdx.x == 0) s_x[0] = c0 > 0 ? ws.runs[s0 + c0 - 1].x : 0;
+    if (threadIdx.x == 1) s_x[cnt + 1] = c0 + cnt < ri.nruns ? ws.runs[s0 + c0 + cnt].x : L;
+    __syncthreads();
+    for (int i = 0; i < cnt; ++i) {
+      if (!s_nx[i]) continue;                 // a Nexus run follows its body run (the grammar)
+      const int body = s_x[i], start = s_x[i + 1], end = s_x[i + 2];
+      const int blen = start - body, K = end - start;
+      const int first = base + s_y[i];        // Nexus tokens of the request before this run
+      for (int j = threadIdx.x; j < K; j += 256) {
+        const int s = static_cast<int>(static_cast<int64_t>(j) * blen / K);
+        const int e = max(static_cast<int>(static_cast<int64_t>(j + 1) * blen / K), s + 1);
+        items[first + j] = make_int4(s0 + start + j, s0 + body + s, s0 + body + e, 0);
+      }
+    }
+    __syncthreads();
   }
 }
 
