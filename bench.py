@@ -151,12 +151,17 @@ def main():
     use_graph = not args.no_graph
     graphs = {}
     if use_graph:
-        # one HIP graph per phase; a step replays the three in order
+        # the step as one HIP graph (prefill, compaction, the 256 decode calls); and one
+        # graph per phase, replayed apart to split a step's time into its phases
         for name, f in phases.items():
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
                 f()
             graphs[name] = g
+        step_graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(step_graph):
+            for f in phases.values():
+                f()
         torch.cuda.synchronize()
         full_graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(full_graph):
@@ -165,13 +170,22 @@ def main():
     stream = torch.cuda.current_stream()
 
     def step(marks=None):
+        if marks: marks[0].record(stream)
+        if use_graph:
+            step_graph.replay()
+        else:
+            for f in phases.values():
+                f()
+        if marks: marks[1].record(stream)
+
+    def phase_split(marks):
         for i, name in enumerate(("prefill", "compact", "decode")):
-            if marks: marks[i].record(stream)
+            marks[i].record(stream)
             if use_graph:
                 graphs[name].replay()
             else:
                 phases[name]()
-        if marks: marks[3].record(stream)
+        marks[3].record(stream)
 
     for _ in range(args.warmup):
         step()
@@ -179,7 +193,7 @@ def main():
     assert db.read_status() == 0, sonic.status_string(db.read_status())
 
     # ---- timed region: exactly K steps ----
-    all_marks = [[ev() for _ in range(4)] for _ in range(args.steps)]
+    all_marks = [[ev() for _ in range(2)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -188,9 +202,16 @@ def main():
     wall = time.perf_counter() - t0
     assert db.read_status() == 0, sonic.status_string(db.read_status())
     ms_per_step = wall * 1e3 / args.steps
-    med = lambda i, j: float(np.median([m[i].elapsed_time(m[j]) for m in all_marks]))
+    step_ms_ev = float(np.median([m[0].elapsed_time(m[1]) for m in all_marks]))
+
+    # ---- the phases of a step, each replayed as its own graph (after the timed region) ----
+    split_marks = [[ev() for _ in range(4)] for _ in range(max(3, args.steps))]
+    for m in split_marks:
+        phase_split(m)
+    torch.cuda.synchronize()
+    assert db.read_status() == 0, sonic.status_string(db.read_status())
+    med = lambda i, j: float(np.median([m[i].elapsed_time(m[j]) for m in split_marks]))
     pf_ms, cp_ms, dc_ms = med(0, 1), med(1, 2), med(2, 3)
-    step_ms_ev = med(0, 3)
 
     # ---- back-to-back launches of the two single-launch phases (no graph-launch gap
     # between phases): their per-launch rate ----

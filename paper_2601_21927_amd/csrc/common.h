@@ -63,10 +63,26 @@ __device__ __forceinline__ void lds_barrier() {
 // prefetches into the other buffers, before each LDS read.  Completion is waited
 // for explicitly (wait_vm) before the data is read.
 __device__ __forceinline__ void dma_row16(const char *src, const uint16_t *dst) {
-  // C-style cast: converting the LDS pointer to its 32-bit address
-  const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
-      reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) uint16_t *)dst)));
+  // the low 32 bits of a generic pointer into LDS are its LDS address
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(dst)));
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds) : "memory", "m0");
+}
+
+// A wave-uniform pointer moved into SGPRs (values loaded through ordinary global
+// loads live in VGPRs even when every lane holds the same one).
+__device__ __forceinline__ const char *uniform_ptr(const char *p) {
+  const uint64_t u = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u >> 32));
+  return reinterpret_cast<const char *>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// The same load with a wave-uniform 64-bit base (in SGPRs) and a 32-bit per-lane
+// byte offset: no per-lane 64-bit address arithmetic.
+// The LDS destination is given as its 32-bit LDS address.
+__device__ __forceinline__ void dma_row16_s(const char *base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(off), "s"(uniform_ptr(base)),
+               "s"(__builtin_amdgcn_readfirstlane(lds)) : "memory", "m0");
 }
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }

@@ -70,24 +70,71 @@ template <int D> __device__ __forceinline__ int swz_v(int r) {
 // first key: their scores are masked, so they contribute exactly zero (a step
 // wholly past the end loads key 0 throughout and is never read).  Wave w issues
 // instructions w, w + G, ... of the INSTS the step needs.
+//
+// Byte offset of a lane's chunk within a step, for instruction ii:
+//   row(ii, lane) * row_bytes + 16 * chunk(ii, lane)
+//     = urow(ii) * row_bytes + (lane_off ^ 16 * xu(ii))
+// with urow and xu wave-uniform and lane_off fixed per lane (the low bits that
+// the chunk XOR touches are below D * 2, where row offsets are zero).  A step
+// whose 64 keys lie in one piece of the list therefore needs no per-lane address
+// arithmetic beyond one XOR: its base row goes into SGPRs.
+template <int D, bool IS_V> __device__ __forceinline__ uint32_t dma_lane_off(int lane, uint32_t row_bytes) {
+  constexpr int DC = D / 8;
+  const int l = lane / DC;     // row within the instruction's rows
+  const int lc = lane % DC;    // chunk slot
+  int lrow = l, lchunk = lc ^ l;
+  if (IS_V) lchunk = lc ^ swz_v<D>(l);
+  else if (D == 64) lrow = (l & 3) + 8 * (l >> 2);
+  return static_cast<uint32_t>(lrow) * row_bytes + 16u * static_cast<uint32_t>(lchunk);
+}
+template <int D, bool IS_V> __device__ __forceinline__ int dma_urow(int ii) {
+  constexpr int ROWS_PER_INST = kWave / (D / 8);
+  if (IS_V) return ii * ROWS_PER_INST;
+  if (D == 128) return 4 * ((ii & ~3) | ((ii & 1) << 1) | ((ii >> 1) & 1));
+  return 4 * (ii & 1) + 16 * (ii >> 1);
+}
+template <int D, bool IS_V> __device__ __forceinline__ uint32_t dma_xu(int ii) {
+  if (IS_V) return 0u;
+  return D == 128 ? 64u * static_cast<uint32_t>(ii & 3) : 16u * static_cast<uint32_t>(ii & 1);
+}
+
 template <int D, int G, bool IS_V>
 __device__ __forceinline__ void stage_tensor(uint16_t *lds_buf, const char *pre_base, const char *req_base,
-                                             uint32_t row_bytes, int wave, int lane, int c, int nv, int npre,
-                                             int seg_shift) {
+                                             uint32_t row_bytes, uint32_t lane_off, int wave, int lane, int c,
+                                             int nv, int npre, int seg_shift) {
   constexpr int DC = D / 8;
   constexpr int ROWS_PER_INST = kWave / DC;
   constexpr int INSTS = kKeyChunk / ROWS_PER_INST;
   constexpr int NJ = (INSTS + G - 1) / G;
+  const int vk0 = c * kKeyChunk;
+  // Every wave issues exactly NJ instructions (so that its wait counts are
+  // static); where G does not divide INSTS, the surplus ones repeat the last
+  // instruction, writing the same bytes to the same LDS rows.
+  if (vk0 + kKeyChunk <= npre || (vk0 >= npre && vk0 + kKeyChunk <= nv)) {
+    // the whole step in one piece: SGPR base row, fixed per-lane offsets
+    const char *sb = vk0 < npre ? pre_base + static_cast<size_t>(vk0) * row_bytes
+                                : req_base + static_cast<size_t>(vk0 + seg_shift) * row_bytes;
+    const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds_buf));
+#pragma unroll
+    for (int jj = 0; jj < NJ; ++jj) {
+      const int ii = min(wave + jj * G, INSTS - 1);
+      // Opaque copies: each instruction's row offset and LDS address are formed
+      // here with two scalar operations instead of being hoisted out of the key
+      // loop into SGPRs (one pair per instruction and buffer would not fit).
+      uint32_t rb = __builtin_amdgcn_readfirstlane(row_bytes), la = __builtin_amdgcn_readfirstlane(lds0);
+      asm volatile("" : "+s"(rb), "+s"(la));
+      dma_row16_s(sb + static_cast<size_t>(static_cast<uint32_t>(dma_urow<D, IS_V>(ii)) * rb),
+                  lane_off ^ dma_xu<D, IS_V>(ii), la + static_cast<uint32_t>(ii * ROWS_PER_INST * D * 2));
+    }
+    return;
+  }
 #pragma unroll
   for (int jj = 0; jj < NJ; ++jj) {
-    // Every wave issues exactly NJ instructions (so that its wait counts are
-    // static); where G does not divide INSTS, the surplus ones repeat the last
-    // instruction, writing the same bytes to the same LDS rows.
     const int ii = min(wave + jj * G, INSTS - 1);
     {
       const int m = ii * ROWS_PER_INST + lane / DC;
       const int r = IS_V ? m : ((m & 32) | perm32(m & 31));
-      int vk = c * kKeyChunk + r;
+      int vk = vk0 + r;
       if (vk >= nv) vk = 0;
       const bool pre = vk < npre;
       const uint32_t chunk_bytes = static_cast<uint32_t>(((lane % DC) ^ (IS_V ? swz_v<D>(m) : swz_k<D>(m))) * 16);
@@ -132,16 +179,26 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, Pr
   const int ti = lane & 15;
   const int v_row_off = 8 * (tq >> 1) + (ti >> 2);      // + 16*ks + 4*h
   const int v_d_off = 16 * (tq & 1) + 4 * (ti & 3);     // + 32*db
+  const uint32_t row_bytes = static_cast<uint32_t>(Hkv) * D * 2;
+  const uint32_t koff_lane = dma_lane_off<D, false>(lane, row_bytes);
+  const uint32_t voff_lane = dma_lane_off<D, true>(lane, row_bytes);
 
   for (;;) {
     if (threadIdx.x == 0) s_item = atomicAdd(&ws.ctrl[8 + xcd], 1) * kNumXcd + xcd;
     __syncthreads();
-    const int item = s_item;
+    const int item = __builtin_amdgcn_readfirstlane(s_item);
     __syncthreads();
     if (item >= nitems) break;
     const int slot = ws.order[item / Hkv];
     const int kvh = item % Hkv;
-    const TileDesc t = ws.tiles[slot];
+    TileDesc t = ws.tiles[slot];
+    t.req = __builtin_amdgcn_readfirstlane(t.req);       // uniform: scalar branches and bases
+    t.p0 = __builtin_amdgcn_readfirstlane(t.p0);
+    t.nrows = __builtin_amdgcn_readfirstlane(t.nrows);
+    t.npre = __builtin_amdgcn_readfirstlane(t.npre);
+    t.seg_start = __builtin_amdgcn_readfirstlane(t.seg_start);
+    t.seg_len = __builtin_amdgcn_readfirstlane(t.seg_len);
+    t.ndiag = __builtin_amdgcn_readfirstlane(t.ndiag);
     const int base = rows.seg_row0[t.req];
     const int64_t pbase = rows.pre_row0 != nullptr ? rows.pre_row0[t.req] : static_cast<int64_t>(base);
     const int h = kvh * G + wave;
@@ -154,17 +211,16 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, Pr
     const size_t phead0 = static_cast<size_t>(pbase) * tok_stride + static_cast<size_t>(kvh) * D;
     // row 0 of the request (and of its prefix rows) for this kv-head; rows are
     // row_bytes apart, and every row of a request lies below 4 GiB from its row 0
-    const char *kreq = reinterpret_cast<const char *>(rows.seg_k + head0);
-    const char *vreq = reinterpret_cast<const char *>(rows.seg_v + head0);
-    const char *kpre = reinterpret_cast<const char *>(rows.pre_k + phead0);
-    const char *vpre = reinterpret_cast<const char *>(rows.pre_v + phead0);
-    const uint32_t row_bytes = static_cast<uint32_t>(tok_stride * 2);
+    const char *kreq = uniform_ptr(reinterpret_cast<const char *>(rows.seg_k + head0));
+    const char *vreq = uniform_ptr(reinterpret_cast<const char *>(rows.seg_v + head0));
+    const char *kpre = uniform_ptr(reinterpret_cast<const char *>(rows.pre_k + phead0));
+    const char *vpre = uniform_ptr(reinterpret_cast<const char *>(rows.pre_v + phead0));
 
     auto stage_k = [&](int c, uint16_t *buf) {
-      stage_tensor<D, G, false>(buf, kpre, kreq, row_bytes, wave, lane, c, nv, npre, seg_shift);
+      stage_tensor<D, G, false>(buf, kpre, kreq, row_bytes, koff_lane, wave, lane, c, nv, npre, seg_shift);
     };
     auto stage_v = [&](int c, uint16_t *buf) {
-      stage_tensor<D, G, true>(buf, vpre, vreq, row_bytes, wave, lane, c, nv, npre, seg_shift);
+      stage_tensor<D, G, true>(buf, vpre, vreq, row_bytes, voff_lane, wave, lane, c, nv, npre, seg_shift);
     };
 
     // Q^T fragments (B operand of S): lane (row n, half g) holds d = 16*ds + 8*g .. +7.
