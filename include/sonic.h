@@ -207,6 +207,8 @@ size_t sonic_role_projection_workspace_bytes(int32_t total_tokens);
  *   workspace       device, >= sonic_role_projection_workspace_bytes(T), 256-byte aligned
  *   dev_status      device int32; while it is non-zero nothing is written
  * Products are accumulated in fp32 from exact bf16 products.
+ * Returns SONIC_ERR_UNSUPPORTED when K is not a multiple of 64, or when x or one
+ * weight set spans more than 4 GiB (T * K * 2 or N * K * 2 bytes).
  */
 int32_t sonic_role_projection(int32_t total_tokens, int32_t in_features, int32_t out_features,
                               const uint8_t *role, const void *x, const void *w_text, const void *w_nexus,

@@ -9,7 +9,7 @@
 #include "common.h"
 
 namespace sonic {
-hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus, int nexus_scope, const int32_t *cu,
+hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int nexus_scope, const int32_t *cu,
                        const uint8_t *role, const int32_t *turn, const uint16_t *k, const uint16_t *v, PrefillWs ws,
                        int32_t *status, hipStream_t stream);
 hipError_t prefill_occupancy(int D, int G, bool stats, int *blocks);
@@ -289,7 +289,7 @@ int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t 
   DeviceInfo *di = nullptr;
   hipError_t e = device_info(&di);
   if (e != hipSuccess) return SONIC_ERR_HIP;
-  e = launch_plan(batch, total_tokens, Hkv, d, di->num_cus, nexus_scope, cu_seqlens, role, turn_id,
+  e = launch_plan(batch, total_tokens, Hkv, d, nexus_scope, cu_seqlens, role, turn_id,
                   static_cast<const uint16_t *>(k), static_cast<const uint16_t *>(v), ws, dev_status, stream);
   if (e != hipSuccess) return SONIC_ERR_HIP;
   const bool stats = nexus_mass != nullptr || key_weight != nullptr;
@@ -413,6 +413,9 @@ int32_t sonic_role_projection(int32_t T, int32_t K, int32_t N, const uint8_t *ro
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   if (T < 0 || K <= 0 || N <= 0 || dev_status == nullptr) return SONIC_ERR_INVALID_ARG;
   if (K % 64 != 0) return SONIC_ERR_UNSUPPORTED;
+  // operand rows are addressed by 32-bit byte offsets
+  if (static_cast<uint64_t>(T) * K * 2 > 0xFFFFFFFFull || static_cast<uint64_t>(N) * K * 2 > 0xFFFFFFFFull)
+    return SONIC_ERR_UNSUPPORTED;
   if (T == 0) return SONIC_OK;
   if (!role || !x || !w_text || !w_nexus || !y || !workspace) return SONIC_ERR_INVALID_ARG;
   if (!aligned(x, 16) || !aligned(w_text, 16) || !aligned(w_nexus, 16) || !aligned(y, 4) ||

@@ -64,6 +64,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_runs_kernel(const int32_t *
                                                                  int total_tokens, int nexus_scope,
                                                                  int32_t *status) {
   __shared__ int lds[kPlanThreads / kWave + 1];
+  __shared__ int lds3[3 * (kPlanThreads / kWave)];
   __shared__ int s_bad;
   __shared__ unsigned long long s_cost;
   const int b = blockIdx.x;
@@ -100,15 +101,14 @@ __global__ __launch_bounds__(kPlanThreads) void plan_runs_kernel(const int32_t *
     if (in && !legal_step(rp, tp, r, t)) s_bad = 1;
     const bool is_pre = in && (r == kSystem || r == kNexus);
     const bool run_start = in && (i == 0 || r != rp || (r == kText && t != tp));
-    int ptot, rtot, ntot;
-    const int prank = block_flag_scan<kPlanThreads>(is_pre, &ptot, lds);
-    const int rrank = block_flag_scan<kPlanThreads>(run_start, &rtot, lds);
-    block_flag_scan<kPlanThreads>(in && r == kNexus, &ntot, lds);
-    if (is_pre) ws.prefix_pos[s + pre_carry + prank] = i;
-    if (run_start) ws.runs[s + run_carry + rrank] = make_int2(i, pre_carry + prank);
-    pre_carry += ptot;
-    run_carry += rtot;
-    nexus_count += ntot;
+    const bool flags[3] = {is_pre, run_start, in && r == kNexus};
+    int below[3], tot[3];
+    block_flags_scan<kPlanThreads, 3>(flags, below, tot, lds3);
+    if (is_pre) ws.prefix_pos[s + pre_carry + below[0]] = i;
+    if (run_start) ws.runs[s + run_carry + below[1]] = make_int2(i, pre_carry + below[0]);
+    pre_carry += tot[0];
+    run_carry += tot[1];
+    nexus_count += tot[2];
   }
   __syncthreads();
   if (s_bad) {
@@ -252,34 +252,63 @@ __global__ __launch_bounds__(kPlanThreads) void plan_order_kernel(const int32_t 
 }
 
 // Prefix copies: row j < S + K_tot of request b's prefix gets the K and V rows
-// of position prefix_pos[cu[b] + j].  One thread per 16-byte piece, pieces of a
-// row contiguous; the request of a row is found by bisection of cu.
+// of position prefix_pos[cu[b] + j].  One wave per kGatherRows consecutive rows of
+// the copy: its first lanes find each row's source (bisection of cu), then the
+// wave copies the rows that have one, all of them in flight at once (a request's
+// prefix rows are the leading rows of its range, so most waves past them copy
+// nothing and end).
 constexpr int kGatherThreads = 256;
+constexpr int kGatherRows = 8;
 
 __global__ __launch_bounds__(kGatherThreads) void gather_prefix_kernel(int batch, const int32_t *__restrict__ cu,
                                                                       const uint16_t *__restrict__ k,
                                                                       const uint16_t *__restrict__ v, PrefillWs ws,
-                                                                      int row_pieces, long long total_pieces,
+                                                                      int row_pieces, int total_rows,
                                                                       const int32_t *status) {
   __shared__ int s_ok;
   if (!block_status_clear(status, &s_ok)) return;
-  const long long stride = static_cast<long long>(gridDim.x) * kGatherThreads;
-  for (long long u = static_cast<long long>(blockIdx.x) * kGatherThreads + threadIdx.x; u < total_pieces;
-       u += stride) {
-    const int g = static_cast<int>(u / row_pieces);
-    const int c = static_cast<int>(u % row_pieces);
-    int lo = 0, hi = batch - 1;        // last b with cu[b] <= g
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (cu[mid] <= g) lo = mid; else hi = mid - 1;
+  const int lane = threadIdx.x % kWave;
+  const int g0 = (blockIdx.x * (kGatherThreads / kWave) + static_cast<int>(threadIdx.x / kWave)) * kGatherRows;
+  if (g0 >= total_rows) return;   // whole waves; no barrier follows
+  int src = -1;                   // lane l < kGatherRows: source row of copy row g0 + l, or -1
+  {
+    const int g = g0 + lane;
+    if (lane < kGatherRows && g < total_rows) {
+      int lo = 0, hi = batch - 1;   // last b with cu[b] <= g
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (cu[mid] <= g) lo = mid; else hi = mid - 1;
+      }
+      const int j = g - cu[lo];
+      const ReqInfo ri = ws.req[lo];
+      if (j >= 0 && j < ri.system + ri.nexus_total) src = cu[lo] + ws.prefix_pos[g];
     }
-    const int j = g - cu[lo];
-    const ReqInfo ri = ws.req[lo];
-    if (j < 0 || j >= ri.system + ri.nexus_total) continue;
-    const size_t src = (static_cast<size_t>(cu[lo]) + ws.prefix_pos[g]) * row_pieces + c;
-    const size_t dst = static_cast<size_t>(g) * row_pieces + c;
-    reinterpret_cast<u32x4 *>(ws.k_pre)[dst] = reinterpret_cast<const u32x4 *>(k)[src];
-    reinterpret_cast<u32x4 *>(ws.v_pre)[dst] = reinterpret_cast<const u32x4 *>(v)[src];
+  }
+  if (__ballot(src >= 0) == 0) return;
+  int sr[kGatherRows];
+#pragma unroll
+  for (int u = 0; u < kGatherRows; ++u) sr[u] = __builtin_amdgcn_readlane(src, u);
+  const u32x4 *__restrict__ k4 = reinterpret_cast<const u32x4 *>(k);
+  const u32x4 *__restrict__ v4 = reinterpret_cast<const u32x4 *>(v);
+  u32x4 *__restrict__ kd = reinterpret_cast<u32x4 *>(ws.k_pre);
+  u32x4 *__restrict__ vd = reinterpret_cast<u32x4 *>(ws.v_pre);
+  for (int c = lane; c < row_pieces; c += kWave) {
+    u32x4 kr[kGatherRows], vr[kGatherRows];
+#pragma unroll
+    for (int u = 0; u < kGatherRows; ++u) {
+      if (sr[u] >= 0) {
+        kr[u] = k4[static_cast<size_t>(sr[u]) * row_pieces + c];
+        vr[u] = v4[static_cast<size_t>(sr[u]) * row_pieces + c];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kGatherRows; ++u) {
+      if (sr[u] >= 0) {
+        const size_t dst = static_cast<size_t>(g0 + u) * row_pieces + c;
+        kd[dst] = kr[u];
+        vd[dst] = vr[u];
+      }
+    }
   }
 }
 
@@ -300,7 +329,7 @@ hipError_t launch_plan_runs(int batch, int total_tokens, const int32_t *cu, cons
   return hipGetLastError();
 }
 
-hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus, int nexus_scope, const int32_t *cu,
+hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int nexus_scope, const int32_t *cu,
                        const uint8_t *role, const int32_t *turn, const uint16_t *k, const uint16_t *v, PrefillWs ws,
                        int32_t *status, hipStream_t stream) {
   plan_runs_kernel<<<dim3(batch), dim3(kPlanThreads), 0, stream>>>(cu, role, turn, ws, total_tokens, nexus_scope,
@@ -308,12 +337,10 @@ hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int num_cus,
   hipError_t e = launch_plan_order(batch, cu, ws, status, stream);
   if (e != hipSuccess) return e;
   const int row_pieces = Hkv * D / 8;
-  const long long total = static_cast<long long>(total_tokens) * row_pieces;
-  long long want = (total + kGatherThreads - 1) / kGatherThreads;
-  const long long cap = static_cast<long long>(num_cus) * 8;
-  const int grid = static_cast<int>(want < cap ? (want > 0 ? want : 1) : cap);
-  gather_prefix_kernel<<<dim3(grid), dim3(kGatherThreads), 0, stream>>>(batch, cu, k, v, ws, row_pieces, total,
-                                                                        status);
+  constexpr int rows_per_block = kGatherThreads / kWave * kGatherRows;
+  const int grid = total_tokens > 0 ? (total_tokens + rows_per_block - 1) / rows_per_block : 1;
+  gather_prefix_kernel<<<dim3(grid), dim3(kGatherThreads), 0, stream>>>(batch, cu, k, v, ws, row_pieces,
+                                                                        total_tokens, status);
   return hipGetLastError();
 }
 

@@ -130,26 +130,32 @@ __global__ __launch_bounds__(kPThreads) void routed_gemm_kernel(
   constexpr int kNW = kPThreads / kWave;
   constexpr int IA = kPM / 8 / kNW, IB = kPN / 8 / kNW;   // per wave and step
   static_assert(IA * kNW * 8 == kPM && IB * kNW * 8 == kPN, "whole instructions per wave");
-  const char *a_src[IA];
-  const char *b_src[IB];
+  // per-lane byte offsets from the operand bases (the host checks that both operands
+  // lie below 4 GiB), with the K step added to the wave-uniform base
+  uint32_t a_off[IA], b_off[IB];
 #pragma unroll
   for (int q = 0; q < IA; ++q) {
     const int r = 8 * (wave * IA + q) + lane / 8;
     const int c = (lane % 8) ^ swz_p(r);
-    a_src[q] = reinterpret_cast<const char *>(x + static_cast<size_t>(rows_lds[r]) * K + 8 * c);
+    a_off[q] = static_cast<uint32_t>(rows_lds[r]) * static_cast<uint32_t>(K) * 2u + 16u * static_cast<uint32_t>(c);
   }
 #pragma unroll
   for (int q = 0; q < IB; ++q) {
     const int r = 8 * (wave * IB + q) + lane / 8;
     const int c = (lane % 8) ^ swz_p(r);
-    b_src[q] = reinterpret_cast<const char *>(w + static_cast<size_t>(min(n0 + r, N - 1)) * K + 8 * c);
+    b_off[q] = static_cast<uint32_t>(min(n0 + r, N - 1)) * static_cast<uint32_t>(K) * 2u +
+               16u * static_cast<uint32_t>(c);
   }
+  const char *xb = uniform_ptr(reinterpret_cast<const char *>(x));
+  const char *wb = uniform_ptr(reinterpret_cast<const char *>(w));
   auto stage = [&](int s, uint16_t *a_buf, uint16_t *b_buf) {
     const size_t koff = static_cast<size_t>(s) * kPK * 2;   // bytes
+    const uint32_t la = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(a_buf));
+    const uint32_t lb = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(b_buf));
 #pragma unroll
-    for (int q = 0; q < IA; ++q) dma_row16(a_src[q] + koff, a_buf + (wave * IA + q) * kWave * 8);
+    for (int q = 0; q < IA; ++q) dma_row16_s(xb + koff, a_off[q], la + (wave * IA + q) * kWave * 16);
 #pragma unroll
-    for (int q = 0; q < IB; ++q) dma_row16(b_src[q] + koff, b_buf + (wave * IB + q) * kWave * 8);
+    for (int q = 0; q < IB; ++q) dma_row16_s(wb + koff, b_off[q], lb + (wave * IB + q) * kWave * 16);
   };
 
   // this wave's (32 kPBM) x (32 kPBN) part of the tile
