@@ -85,19 +85,33 @@ __global__ __launch_bounds__(kPlanThreads) void plan_runs_kernel(const int32_t *
   // with the number of prefix rows before each.  In a well-formed request the
   // system rows come first, so the prefix is the system prompt followed by the
   // Nexus tokens.
+  // The next 1024 tokens are requested before the current ones are counted, so
+  // their load latency overlaps the scan (whose barriers wait for LDS only).
   int pre_carry = 0, run_carry = 0, nexus_count = 0;
-  for (int base = 0; base < L; base += kPlanThreads) {
+  // A token's predecessor comes from the lane below; lane 0 of each wave loads its own.
+  const int lane = threadIdx.x % kWave;
+  auto fetch = [&](int base, int &r, int &t, int &rp, int &tp) {
     const int i = base + threadIdx.x;
-    const bool in = i < L;
-    int r = -1, t = 0, rp = -1, tp = 0;
-    if (in) {
+    r = -1, t = 0, rp = -1, tp = 0;
+    if (i < L) {
       r = role[s + i];
       t = turn[s + i];
-      if (i > 0) {
+      if (lane == 0 && i > 0) {
         rp = role[s + i - 1];
         tp = turn[s + i - 1];
       }
     }
+  };
+  int nr, nt, nrp, ntp;
+  fetch(0, nr, nt, nrp, ntp);
+  for (int base = 0; base < L; base += kPlanThreads) {
+    const int i = base + threadIdx.x;
+    const bool in = i < L;
+    const int r = nr, t = nt;
+    const int up_r = __shfl_up(r, 1), up_t = __shfl_up(t, 1);
+    const int rp = lane == 0 ? nrp : (i > 0 ? up_r : -1);
+    const int tp = lane == 0 ? ntp : (i > 0 ? up_t : 0);
+    if (base + kPlanThreads < L) fetch(base + kPlanThreads, nr, nt, nrp, ntp);
     if (in && !legal_step(rp, tp, r, t)) s_bad = 1;
     const bool is_pre = in && (r == kSystem || r == kNexus);
     const bool run_start = in && (i == 0 || r != rp || (r == kText && t != tp));

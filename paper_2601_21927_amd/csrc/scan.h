@@ -42,6 +42,8 @@ __device__ __forceinline__ int block_flag_scan(bool flag, int *total, int *lds) 
 // below[f] = threads before this one with flag f set, total[f] = the workgroup's
 // count.  Two barriers for all NF flags; every thread sums the per-wave counts
 // it needs itself (broadcast LDS reads), so no thread walks the waves serially.
+// The barriers wait for LDS only: global loads in flight (a prefetch) stay in
+// flight, and global stores made before the scan are not ordered by it.
 // `lds` must hold NF * NT/64 ints.
 template <int NT, int NF>
 __device__ __forceinline__ void block_flags_scan(const bool (&flag)[NF], int (&below)[NF], int (&total)[NF],
@@ -55,7 +57,7 @@ __device__ __forceinline__ void block_flags_scan(const bool (&flag)[NF], int (&b
     below[f] = lanes_below(m);
     if (lane == 0) lds[f * NW + w] = __popcll(m);
   }
-  __syncthreads();
+  lds_barrier();
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
     int before = 0, tot = 0;
@@ -68,7 +70,7 @@ __device__ __forceinline__ void block_flags_scan(const bool (&flag)[NF], int (&b
     below[f] += before;
     total[f] = tot;
   }
-  __syncthreads();
+  lds_barrier();
 }
 
 // Exclusive prefix sum of a non-negative int over an NT-thread workgroup.
