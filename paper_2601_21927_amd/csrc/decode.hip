@@ -398,10 +398,12 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
 }
 
 // Splits per (request, kv-head): about 256 workgroups (one per CU), each of at
-// least 256 rows; one split when there are that many pairs already.
+// least 256 rows.  With that many pairs already, one split, or two when the
+// longest context reaches 2048 rows (so that the longest pair does not outlast
+// the rest of the call when lengths are uneven).
 int decode_splits(int batch, int Hkv, int max_ctx) {
   const long pairs = static_cast<long>(batch) * Hkv;
-  if (pairs >= 256) return 1;
+  if (pairs >= 256) return max_ctx >= 2048 ? 2 : 1;
   long s = (256 + pairs - 1) / pairs;
   const long by_rows = (static_cast<long>(max_ctx) + 255) / 256;
   if (s > by_rows) s = by_rows;
