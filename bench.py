@@ -64,6 +64,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying a HIP graph")
     ap.add_argument("--decode-steps", type=int, default=256)
+    ap.add_argument("--decode-workloads", type=lambda v: [int(x) for x in v.split(",") if x], default=[],
+                    help="also time the compressed decode loop of these workloads (e.g. 3,4,5)")
     return ap.parse_args()
 
 
@@ -384,6 +386,54 @@ def main():
     rc_bytes = float(body_rows + rc_n) * rc_Dm * 2 + rc_n * (rc_Dm * 4 + 8)
     del rc_h
 
+    # ---- optional: the compressed decode loop of other workloads (their whole step count,
+    # one graph, from the freshly compacted cache) ----
+    dec_other = {}
+    for wl in args.decode_workloads:
+        ob = W.workload(wl)
+        odb = SonicBatch(ob.role, ob.turn_id, ob.cu_seqlens, None, ob.k, ob.v, device=dev)
+        okept = np.array([l.system + sum(l.nexus) + l.current for l in ob.layouts], np.int64)
+        ost = ob.decode_steps
+        oc = odb.alloc_cache(okept + ost)
+        omc = int((okept + ost).max())
+        oq, okn, ovn = (bf16_to_device(x, dev) for x in (ob.dec_q, ob.dec_k, ob.dec_v))
+        oout = torch.empty((ob.batch, ob.num_q_heads, ob.head_dim), dtype=torch.float32, device=dev)
+        assert odb.compact() == sonic.OK
+        assert oc.decode(oq[0], okn[0], ovn[0], oout, odb.status, omc) == sonic.OK   # allocates the workspace
+
+        def oloop():
+            for t in range(ost):
+                st = oc.decode(oq[t], okn[t], ovn[t], oout, odb.status, omc)
+                assert st == sonic.OK, sonic.status_string(st)
+        og = None
+        if use_graph:
+            og = torch.cuda.CUDAGraph()
+            assert odb.compact() == sonic.OK
+            with torch.cuda.graph(og):
+                oloop()
+        ots = []
+        for _ in range(3):
+            assert odb.compact() == sonic.OK
+            a, b_ = ev(), ev()
+            a.record(stream)
+            if use_graph:
+                og.replay()
+            else:
+                oloop()
+            b_.record(stream)
+            torch.cuda.synchronize()
+            ots.append(a.elapsed_time(b_))
+        assert odb.read_status() == 0
+        oms = float(np.median(ots))
+        octx = okept[None, :].astype(np.float64) + np.arange(1, ost + 1)[:, None]
+        obytes = float(octx.sum()) * ob.num_kv_heads * ob.head_dim * 2 * 2
+        dec_other[f"workload{wl}"] = {
+            "batch": ob.batch, "steps": ost, "us_per_step": round(oms * 1e3 / ost, 2),
+            "tok_s": round(ob.batch * ost / (oms * 1e-3), 1), "gbs": round(obytes / (oms * 1e-3) / 1e9, 1),
+            "frac_hbm_peak": round(obytes / (oms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+        del og, oc, odb, oq, okn, ovn
+        torch.cuda.synchronize()
+
     # ---- algorithmic work ----
     row_bytes = Hkv * d * 2                       # one token's K (or V) over all kv-heads, bf16
     compact_bytes = float(kept.sum()) * row_bytes * 2 * 2 + batch.total_tokens + float(kept.sum()) * 4
@@ -461,6 +511,8 @@ def main():
                  "recon_targets": f"{rc_n} Nexus tokens, hidden size {rc_Dm}"},
         "roofline": roof,
     }
+    if dec_other:
+        rec["decode_other_workloads"] = dec_other
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(batch, kept)
     print(json.dumps(rec), flush=True)
