@@ -559,11 +559,70 @@ def cpu_baseline(batch, kept):
             OD.decode_step(batch.dec_q[mid + t, b], kctx, vctx, batch.dec_k[mid + t, b], batch.dec_v[mid + t, b])
     t_dec = (time.perf_counter() - t0) / (B * dec_per_req) * B * steps
     total = t_pre + t_cmp + t_dec
+    widened = widened_rows_oracle(batch)
     return {"value": round(B * steps / total, 3), "unit": "tok/s", "cores": cores, "kind": "oracle",
             "sample": f"fp64 oracle: {rows_per_req} prefill rows of each of the {B} requests (scaled to "
                       f"{batch.total_tokens} rows), compaction of the whole batch, {dec_per_req} decode steps of each "
                       f"request from mid-loop context (scaled to {B}x{steps}); estimated step time {total:.1f} s",
-            "prefill_s_est": round(t_pre, 2), "compact_s_est": round(t_cmp, 3), "decode_s_est": round(t_dec, 2)}
+            "prefill_s_est": round(t_pre, 2), "compact_s_est": round(t_cmp, 3), "decode_s_est": round(t_dec, 2),
+            "widened_rows": widened}
+
+
+def widened_rows_oracle(batch):
+    """The fp64 oracle of the four widened rows on bounded samples of the bench's shapes
+    (request 0 of the batch, or a block of rows), each scaled to the bench's whole call.
+    Inputs are seeded bf16 bit patterns of those shapes; only the time is used."""
+    from oracle import extend as OE
+    from oracle import projection as OP
+    from oracle import recon as OR
+    from oracle import stats as OS
+    import workloads as W
+    rng = np.random.default_rng(11)
+    bits = lambda shape, sc=1.0: W.f32_to_bf16_bits((rng.standard_normal(shape) * sc).astype(np.float32))
+    B = batch.batch
+    cu = batch.cu_seqlens
+    s0, e0 = int(cu[0]), int(cu[1])
+    lay = batch.layouts[0]
+    role0, turn0 = batch.role[s0:e0], batch.turn_id[s0:e0]
+    res = {}
+    # next-turn Nexus step: the last segment's Nexus rows over a cache of kept + decoded rows
+    kn = lay.nexus[-1]
+    cache_rows = lay.system + sum(lay.nexus) + lay.current + batch.decode_steps
+    q_new, k_new, v_new = bits((kn, batch.num_q_heads, batch.head_dim)), bits((kn, batch.num_kv_heads, batch.head_dim)), \
+        bits((kn, batch.num_kv_heads, batch.head_dim))
+    kc, vc = batch.k[s0:s0 + cache_rows], batch.v[s0:s0 + cache_rows]
+    t0 = time.perf_counter()
+    OE.extend_request(q_new, k_new, v_new, kc, vc, lay.system + sum(lay.nexus[:-1]))
+    res["next_turn_nexus_ms_est"] = round((time.perf_counter() - t0) * B * 1e3, 1)
+    # attention statistics: Nexus mass of 200 rows of request 0 (scaled to every row), key weights of request 0
+    rows = np.linspace(0, e0 - s0 - 1, 200).astype(np.int64)
+    t0 = time.perf_counter()
+    OS.nexus_mass(batch.q[s0:e0], batch.k[s0:e0], role0, turn0, rows=rows)
+    t_m = (time.perf_counter() - t0) * batch.total_tokens / len(rows)
+    t0 = time.perf_counter()
+    OS.key_weight(batch.q[s0:e0], batch.k[s0:e0], role0, turn0)
+    t_w = (time.perf_counter() - t0) * B
+    res["attention_statistics_ms_est"] = round((t_m + t_w) * 1e3, 1)
+    # role-routed QKV projection (K = 4096, N = Hq d + 2 Hkv d): 128 and 640 rows give the
+    # per-row and the per-call (weight widening) parts, extrapolated to every row
+    K, N = 4096, (batch.num_q_heads + 2 * batch.num_kv_heads) * batch.head_dim
+    x, wt, wn = bits((640, K)), bits((N, K), 0.02), bits((N, K), 0.02)
+    OP.role_routed_linear(x[:128], batch.role[s0:s0 + 128], wt, wn)   # warm (threads, pages)
+    tp = []
+    for n in (128, 640):
+        t0 = time.perf_counter()
+        OP.role_routed_linear(x[:n], batch.role[s0:s0 + n], wt, wn)
+        tp.append(time.perf_counter() - t0)
+    per_row = max(tp[1] - tp[0], 0.0) / 512
+    res["role_projection_qkv_ms_est"] = round((max(tp[0] - 128 * per_row, 0.0) + per_row * batch.total_tokens) * 1e3, 1)
+    # reconstruction targets, hidden size 4096: request 0, scaled to the batch
+    h = bits((e0 - s0, 4096))
+    t0 = time.perf_counter()
+    OR.recon_request(h, role0, turn0)
+    res["recon_targets_ms_est"] = round((time.perf_counter() - t0) * B * 1e3, 1)
+    res["sample"] = ("request 0 of the batch (next-turn step, key weights, reconstruction), 200 rows of it "
+                     "(Nexus mass), 128 and 640 rows (projection), each scaled to the bench's whole call")
+    return res
 
 
 
