@@ -224,7 +224,6 @@ static size_t prefill_ws_layout(int32_t batch, int32_t T, int32_t Hq, int32_t Hk
   const size_t B1 = static_cast<size_t>(batch > 0 ? batch : 1);
   const size_t T1 = static_cast<size_t>(T > 0 ? T : 1);
   char *req = take(sizeof(ReqInfo) * B1);
-  char *req_off = take(sizeof(int32_t) * B1);
   char *ppos = take(sizeof(int32_t) * T1);
   char *runs = take(sizeof(int2) * T1);
   char *tiles = take(sizeof(TileDesc) * T1);
@@ -240,7 +239,6 @@ static size_t prefill_ws_layout(int32_t batch, int32_t T, int32_t Hq, int32_t Hk
   char *ncur = take(sizeof(int32_t) * B1);
   if (ws) {
     ws->req = reinterpret_cast<ReqInfo *>(req);
-    ws->req_off = reinterpret_cast<int32_t *>(req_off);
     ws->prefix_pos = reinterpret_cast<int32_t *>(ppos);
     ws->runs = reinterpret_cast<int2 *>(runs);
     ws->tiles = reinterpret_cast<TileDesc *>(tiles);
@@ -317,14 +315,12 @@ static size_t extend_ws_layout(int32_t batch, int32_t total_new, PrefillWs *ws, 
   const size_t B1 = static_cast<size_t>(batch > 0 ? batch : 1);
   const size_t N1 = static_cast<size_t>(total_new > 0 ? total_new : 1);
   char *req = take(sizeof(ReqInfo) * B1);
-  char *req_off = take(sizeof(int32_t) * B1);
   char *tiles = take(sizeof(TileDesc) * N1);
   char *order = take(sizeof(int32_t) * N1);
   char *ctrl = take(sizeof(int32_t) * 16);
   if (ws) {
     *ws = PrefillWs{};
     ws->req = reinterpret_cast<ReqInfo *>(req);
-    ws->req_off = reinterpret_cast<int32_t *>(req_off);
     ws->tiles = reinterpret_cast<TileDesc *>(tiles);
     ws->order = reinterpret_cast<int32_t *>(order);
     ws->ctrl = reinterpret_cast<int32_t *>(ctrl);

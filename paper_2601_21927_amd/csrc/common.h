@@ -151,7 +151,6 @@ struct AttnRows {
 // Device workspace of the prefill, carved from one caller buffer.
 struct PrefillWs {
   ReqInfo *req;        // [B]
-  int32_t *req_off;    // [B]  first slot of request b in `order`
   int32_t *prefix_pos; // [T]  request b's prefix rows (system, then Nexus) at offset cu[b]: positions
   int2 *runs;          // [T]  (run start, Nexus count before it) at offset cu[b]
   TileDesc *tiles;     // [T]  request b's descriptors at offset cu[b]

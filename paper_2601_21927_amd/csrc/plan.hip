@@ -199,56 +199,46 @@ __global__ __launch_bounds__(kPlanThreads) void plan_runs_kernel(const int32_t *
   if (threadIdx.x == 0) ws.req[b] = ReqInfo{tile_carry, S, k_tot, nruns, static_cast<int64_t>(s_cost), 0};
 }
 
-// One workgroup: rank the requests by decreasing cost (index order beyond
-// kRankMax requests), give each its first slot in `order`, reset the queues.
-constexpr int kRankMax = 1024;
-
-__global__ __launch_bounds__(kPlanThreads) void plan_rank_kernel(int batch, PrefillWs ws, const int32_t *status) {
-  __shared__ long long cost[kRankMax];
-  __shared__ int sorted[kRankMax];
-  __shared__ int lds[kPlanThreads / kWave + 1];
-  __shared__ int s_ok;
-  const bool ok = block_status_clear(status, &s_ok);
-  const bool ranked = batch <= kRankMax;
-  if (ranked) {
-    for (int b = threadIdx.x; b < batch; b += kPlanThreads) cost[b] = ws.req[b].cost;
-    __syncthreads();
-    for (int b = threadIdx.x; b < batch; b += kPlanThreads) {
-      const long long c = cost[b];
-      int rank = 0;
-      for (int j = 0; j < batch; ++j) rank += (cost[j] > c || (cost[j] == c && j < b)) ? 1 : 0;
-      sorted[rank] = b;
-    }
-    __syncthreads();
-  }
-  int carry = 0;
-  for (int base = 0; base < batch; base += kPlanThreads) {
-    const int i = base + threadIdx.x;
-    const int b = i < batch ? (ranked ? sorted[i] : i) : 0;
-    const int n = i < batch ? ws.req[b].ntiles : 0;
-    int tot;
-    const int off = block_int_scan<kPlanThreads>(n, &tot, lds);
-    if (i < batch) ws.req_off[b] = carry + off;
-    carry += tot;
-  }
-  if (threadIdx.x == 0) ws.ctrl[0] = ok ? carry : 0;
-  if (threadIdx.x < kNumXcd) ws.ctrl[8 + threadIdx.x] = 0;
-}
-
 // One workgroup per request: its descriptors by decreasing cost (a histogram
-// sort over kCostBuckets cost values, larger costs share the last bucket).
-__global__ __launch_bounds__(kPlanThreads) void plan_order_kernel(const int32_t *__restrict__ cu, PrefillWs ws,
-                                                                  const int32_t *status) {
+// sort over kCostBuckets cost values, larger costs share the last bucket), from
+// its first slot in `order`.  Requests run by decreasing total cost (ties by
+// index), so that first slot is the number of descriptors of the requests ranked
+// before it: a workgroup sum over the batch, no global sort.  Workgroup 0 also
+// writes the descriptor count and resets the queues.
+__global__ __launch_bounds__(kPlanThreads) void plan_order_kernel(int batch, const int32_t *__restrict__ cu,
+                                                                  PrefillWs ws, const int32_t *status) {
   __shared__ int hist[kCostBuckets];
   __shared__ int lds[kPlanThreads / kWave + 1];
   __shared__ int s_ok;
   static_assert(kCostBuckets == kPlanThreads, "one histogram bucket per thread");
   const int b = blockIdx.x;
   hist[threadIdx.x] = 0;
-  if (!block_status_clear(status, &s_ok)) return;
+  const bool ok = block_status_clear(status, &s_ok);
+  if (b == 0 && threadIdx.x < kNumXcd) ws.ctrl[8 + threadIdx.x] = 0;
+  if (!ok) {
+    if (b == 0 && threadIdx.x == 0) ws.ctrl[0] = 0;
+    return;
+  }
+  const int64_t cb = ws.req[b].cost;
+  int before = 0, all = 0;
+  for (int j0 = 0; j0 < batch; j0 += kPlanThreads) {
+    const int j = j0 + threadIdx.x;
+    int nt_j = 0, nb = 0;
+    if (j < batch) {
+      const ReqInfo rj = ws.req[j];
+      nt_j = rj.ntiles;
+      nb = (rj.cost > cb || (rj.cost == cb && j < b)) ? nt_j : 0;
+    }
+    int t0, t1;
+    block_int_scan<kPlanThreads>(nb, &t0, lds);
+    block_int_scan<kPlanThreads>(nt_j, &t1, lds);
+    before += t0;
+    all += t1;
+  }
+  if (b == 0 && threadIdx.x == 0) ws.ctrl[0] = all;
   const int nt = ws.req[b].ntiles;
   const int base = cu[b];
-  const int dst = ws.req_off[b];
+  const int dst = before;
   for (int j = threadIdx.x; j < nt; j += kPlanThreads) {
     const int c = min(tile_cost(ws.tiles[base + j]), kCostBuckets - 1);
     atomicAdd(&hist[kCostBuckets - 1 - c], 1);
@@ -329,8 +319,7 @@ __global__ __launch_bounds__(kGatherThreads) void gather_prefix_kernel(int batch
 // Work order of the descriptors of a batch (request b's at offset cu[b] of ws.tiles)
 // and reset queues; shared by the prefill and the next-turn Nexus step.
 hipError_t launch_plan_order(int batch, const int32_t *cu, PrefillWs ws, int32_t *status, hipStream_t stream) {
-  plan_rank_kernel<<<dim3(1), dim3(kPlanThreads), 0, stream>>>(batch, ws, status);
-  plan_order_kernel<<<dim3(batch), dim3(kPlanThreads), 0, stream>>>(cu, ws, status);
+  plan_order_kernel<<<dim3(batch), dim3(kPlanThreads), 0, stream>>>(batch, cu, ws, status);
   return hipGetLastError();
 }
 
