@@ -296,8 +296,7 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
       x[i] = vis ? sacc[i] * scale_log2 : -INFINITY;
       mloc = fmaxf(mloc, x[i]);
     }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    mloc = pair32_max(pair16_max(mloc));
     if (__any(mloc > m_run + 8.f)) {   // rescale only when the max grows by more than 2^8
       const float m_new = fmaxf(m_run, mloc);
       const float corr = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
@@ -348,8 +347,7 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
   }
 
   // ---- merge: columns across the four quarters, then the waves through LDS ----
-  l_run += __shfl_xor(l_run, 16);
-  l_run += __shfl_xor(l_run, 32);
+  l_run = pair32_add(pair16_add(l_run));
   if (quarter == 0) {
     m_lds[wave][col] = m_run;
     l_lds[wave][col] = l_run;

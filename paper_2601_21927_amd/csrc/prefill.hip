@@ -299,7 +299,7 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, Pr
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int e = 0; e < 16; ++e) mloc = fmaxf(mloc, sacc[kb][e]);
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32)) * scale_log2;
+      mloc = pair32_max(mloc) * scale_log2;
       if (__any(mloc > m_run + kLazy)) {
         const float m_new = fmaxf(m_run, mloc);
         const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -368,10 +368,10 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, Pr
     }
 
     // ---- normalise and store: lane (n, g) holds d = 32*db + 8*i + 4*g + (0..3) ----
-    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    const float l_tot = pair32_add(l_run);
     const float inv = 1.f / l_tot;
     if (STATS) {
-      const float n_tot = l_nex + __shfl_xor(l_nex, 32);
+      const float n_tot = pair32_add(l_nex);
       if (n < t.nrows && g == 0) {
         const size_t idx = static_cast<size_t>(base + t.p0 + n) * Hq + h;
         if (rows.nexus_mass != nullptr) rows.nexus_mass[idx] = n_tot * inv;

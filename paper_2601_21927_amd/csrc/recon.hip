@@ -101,8 +101,9 @@ __device__ __forceinline__ void block_sum(float (&v)[R], float (*red)[kReconWave
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
 #pragma unroll
   for (int k = 0; k < R; ++k) {
+    v[k] = pair16_add(pair32_add(v[k]));
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v[k] += __shfl_xor(v[k], o);
+    for (int o = 8; o > 0; o >>= 1) v[k] += __shfl_xor(v[k], o);
   }
   if (lane == 0)
 #pragma unroll

@@ -142,7 +142,7 @@ __global__ __launch_bounds__(G * kWave) void key_weight_kernel(const int32_t *__
         v += __shfl_xor(v, 2);
         v += __shfl_xor(v, 4);
         v += __shfl_xor(v, 8);
-        v += __shfl_xor(v, 16);
+        v = pair16_add(v);
         if (n == 0) red[wave][kb * 32 + 8 * (e >> 2) + 4 * g + (e & 3)] = v;
       }
     __syncthreads();
