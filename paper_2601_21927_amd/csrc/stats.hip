@@ -132,19 +132,38 @@ __global__ __launch_bounds__(G * kWave) void key_weight_kernel(const int32_t *__
         }
       }
     }
-    // sum over the 32 rows (lanes with the same half g), then over the waves
+    // Sum over the 32 rows (lanes with the same half g), then over the waves.  The 32
+    // values E = 16 kb + e of a lane are summed over its 32 lanes by halving: at the
+    // stage of lane bit m, a lane keeps the half of its values whose E bit matches its
+    // own bit m and adds the partner's copy of that half, so after five stages lane n
+    // holds the sum for E = n (31 exchanges instead of 160).  The first stage (bit 4)
+    // is one v_permlane16_swap per pair (E, E + 16): it leaves every lane its pair's
+    // kept value and the partner's in two registers.
+    float v16[16];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int e = 0; e < 16; ++e) {
+      const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(wacc[0][e]), __float_as_uint(wacc[1][e]),
+                                                      false, false);
+      v16[e] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    }
+    auto halve = [&](auto &src, auto &dst, int half, int m) {
+      const bool hi = (n & m) != 0;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float v = wacc[kb][e];
-        v += __shfl_xor(v, 1);
-        v += __shfl_xor(v, 2);
-        v += __shfl_xor(v, 4);
-        v += __shfl_xor(v, 8);
-        v = pair16_add(v);
-        if (n == 0) red[wave][kb * 32 + 8 * (e >> 2) + 4 * g + (e & 3)] = v;
+      for (int i = 0; i < half; ++i) {
+        const float keep = hi ? src[i + half] : src[i];
+        const float send = hi ? src[i] : src[i + half];
+        dst[i] = keep + __shfl_xor(send, m);
       }
+    };
+    float v8[8], v4[4], v2[2], v1[1];
+    halve(v16, v8, 8, 8);
+    halve(v8, v4, 4, 4);
+    halve(v4, v2, 2, 2);
+    halve(v2, v1, 1, 1);
+    {
+      const int E = n, kb = E >> 4, e = E & 15;
+      red[wave][kb * 32 + 8 * (e >> 2) + 4 * g + (e & 3)] = v1[0];
+    }
     __syncthreads();
     if (threadIdx.x < kWBlock) {
       const int j = j0 + threadIdx.x;
