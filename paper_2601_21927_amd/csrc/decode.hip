@@ -111,8 +111,13 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
   const int b = blockIdx.z;
   const int Hq = Hkv * G;
   const int len = cache_len[b];
+  const int cap = row_cap[b];
+  // the request's first cache row is requested with its length (one round trip for
+  // both, not a second one after the capacity check)
+  const int64_t base = row_off[b];
+  asm volatile("" ::"s"(base));
   const int n_ctx = len + 1;
-  if (n_ctx > row_cap[b] || n_ctx > max_ctx) {   // uniform over the request: no append, no output
+  if (n_ctx > cap || n_ctx > max_ctx) {   // uniform over the request: no append, no output
     if (split == 0 && kvh == 0 && threadIdx.x == 0) raise_status(status, SONIC_ERR_CAPACITY);
     return;
   }
@@ -183,7 +188,6 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
   const int r_begin = split * R;
   const int r_end = min(n_ctx, r_begin + R);
   const int ngroups = (r_end - r_begin + kGroupRows - 1) / kGroupRows;
-  const int64_t base = row_off[b];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = threadIdx.x % kWave;
   const int col = lane & 15;       // score column (q-head) / value-product column

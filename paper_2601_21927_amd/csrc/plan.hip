@@ -256,62 +256,64 @@ __global__ __launch_bounds__(kPlanThreads) void plan_order_kernel(int batch, con
 }
 
 // Prefix copies: row j < S + K_tot of request b's prefix gets the K and V rows
-// of position prefix_pos[cu[b] + j].  One wave per kGatherRows consecutive rows of
-// the copy: its first lanes find each row's source (bisection of cu), then the
-// wave copies the rows that have one, all of them in flight at once (a request's
-// prefix rows are the leading rows of its range, so most waves past them copy
-// nothing and end).
+// of position prefix_pos[cu[b] + j].  Workgroups gx*b .. gx*b + gx-1 copy request
+// b's prefix, one wave per kGatherRows consecutive rows, waves striding over the
+// prefix.  The wave's first lanes read the rows' positions, then every
+// lane has all of its 16-byte pieces of those rows in flight before it stores
+// (kGatherPieces per row and tensor at a time).
 constexpr int kGatherThreads = 256;
-constexpr int kGatherRows = 8;
+constexpr int kGatherWaves = kGatherThreads / kWave;
+constexpr int kGatherRows = 4;
+constexpr int kGatherPieces = 2;
 
-__global__ __launch_bounds__(kGatherThreads) void gather_prefix_kernel(int batch, const int32_t *__restrict__ cu,
+__global__ __launch_bounds__(kGatherThreads) void gather_prefix_kernel(const int32_t *__restrict__ cu,
                                                                       const uint16_t *__restrict__ k,
                                                                       const uint16_t *__restrict__ v, PrefillWs ws,
-                                                                      int row_pieces, int total_rows,
+                                                                      int row_pieces, int gx,
                                                                       const int32_t *status) {
   __shared__ int s_ok;
   if (!block_status_clear(status, &s_ok)) return;
+  const int b = blockIdx.x / gx;
+  const int bx = blockIdx.x % gx;
+  const int s0 = cu[b];
+  const ReqInfo ri = ws.req[b];
+  const int npre = ri.system + ri.nexus_total;
   const int lane = threadIdx.x % kWave;
-  const int g0 = (blockIdx.x * (kGatherThreads / kWave) + static_cast<int>(threadIdx.x / kWave)) * kGatherRows;
-  if (g0 >= total_rows) return;   // whole waves; no barrier follows
-  int src = -1;                   // lane l < kGatherRows: source row of copy row g0 + l, or -1
-  {
-    const int g = g0 + lane;
-    if (lane < kGatherRows && g < total_rows) {
-      int lo = 0, hi = batch - 1;   // last b with cu[b] <= g
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (cu[mid] <= g) lo = mid; else hi = mid - 1;
-      }
-      const int j = g - cu[lo];
-      const ReqInfo ri = ws.req[lo];
-      if (j >= 0 && j < ri.system + ri.nexus_total) src = cu[lo] + ws.prefix_pos[g];
-    }
-  }
-  if (__ballot(src >= 0) == 0) return;
-  int sr[kGatherRows];
-#pragma unroll
-  for (int u = 0; u < kGatherRows; ++u) sr[u] = __builtin_amdgcn_readlane(src, u);
+  const int wave = threadIdx.x / kWave;
   const u32x4 *__restrict__ k4 = reinterpret_cast<const u32x4 *>(k);
   const u32x4 *__restrict__ v4 = reinterpret_cast<const u32x4 *>(v);
   u32x4 *__restrict__ kd = reinterpret_cast<u32x4 *>(ws.k_pre);
   u32x4 *__restrict__ vd = reinterpret_cast<u32x4 *>(ws.v_pre);
-  for (int c = lane; c < row_pieces; c += kWave) {
-    u32x4 kr[kGatherRows], vr[kGatherRows];
+  const int stride = gx * kGatherWaves * kGatherRows;
+  for (int j0 = (bx * kGatherWaves + wave) * kGatherRows; j0 < npre; j0 += stride) {
+    int src = -1;   // lane u < kGatherRows: source row of copy row j0 + u, or -1 past the prefix
+    if (lane < kGatherRows && j0 + lane < npre) src = s0 + ws.prefix_pos[s0 + j0 + lane];
+    int sr[kGatherRows];
 #pragma unroll
-    for (int u = 0; u < kGatherRows; ++u) {
-      if (sr[u] >= 0) {
-        kr[u] = k4[static_cast<size_t>(sr[u]) * row_pieces + c];
-        vr[u] = v4[static_cast<size_t>(sr[u]) * row_pieces + c];
-      }
-    }
+    for (int u = 0; u < kGatherRows; ++u) sr[u] = __builtin_amdgcn_readlane(src, u);
+    for (int c0 = 0; c0 < row_pieces; c0 += kGatherPieces * kWave) {
+      u32x4 kr[kGatherRows][kGatherPieces], vr[kGatherRows][kGatherPieces];
 #pragma unroll
-    for (int u = 0; u < kGatherRows; ++u) {
-      if (sr[u] >= 0) {
-        const size_t dst = static_cast<size_t>(g0 + u) * row_pieces + c;
-        kd[dst] = kr[u];
-        vd[dst] = vr[u];
-      }
+      for (int u = 0; u < kGatherRows; ++u)
+#pragma unroll
+        for (int p = 0; p < kGatherPieces; ++p) {
+          const int c = c0 + p * kWave + lane;
+          if (sr[u] >= 0 && c < row_pieces) {
+            kr[u][p] = k4[static_cast<size_t>(sr[u]) * row_pieces + c];
+            vr[u][p] = v4[static_cast<size_t>(sr[u]) * row_pieces + c];
+          }
+        }
+#pragma unroll
+      for (int u = 0; u < kGatherRows; ++u)
+#pragma unroll
+        for (int p = 0; p < kGatherPieces; ++p) {
+          const int c = c0 + p * kWave + lane;
+          if (sr[u] >= 0 && c < row_pieces) {
+            const size_t dst = static_cast<size_t>(s0 + j0 + u) * row_pieces + c;
+            kd[dst] = kr[u][p];
+            vd[dst] = vr[u][p];
+          }
+        }
     }
   }
 }
@@ -340,10 +342,12 @@ hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int nexus_sc
   hipError_t e = launch_plan_order(batch, cu, ws, status, stream);
   if (e != hipSuccess) return e;
   const int row_pieces = Hkv * D / 8;
-  constexpr int rows_per_block = kGatherThreads / kWave * kGatherRows;
-  const int grid = total_tokens > 0 ? (total_tokens + rows_per_block - 1) / rows_per_block : 1;
-  gather_prefix_kernel<<<dim3(grid), dim3(kGatherThreads), 0, stream>>>(batch, cu, k, v, ws, row_pieces,
-                                                                        total_tokens, status);
+  // about 2048 workgroups over the batch, none with nothing but rows past every prefix
+  constexpr int rows_per_block = kGatherWaves * kGatherRows;
+  const int by_rows = (total_tokens + rows_per_block - 1) / rows_per_block;
+  const int gx = max(1, min((2048 + batch - 1) / batch, by_rows));
+  gather_prefix_kernel<<<dim3(gx * batch), dim3(kGatherThreads), 0, stream>>>(cu, k, v, ws, row_pieces, gx,
+                                                                              status);
   return hipGetLastError();
 }
 

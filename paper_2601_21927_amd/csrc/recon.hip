@@ -11,7 +11,8 @@
 // kernel numbers the Nexus tokens of the batch (position order) and one lists,
 // per Nexus token, its position and its interval.  The pooling is HBM-bound:
 // one workgroup per Nexus token (persistent grid) reads the Nexus row and its
-// interval's rows once, four rows per step: each thread holds 8-element chunks
+// interval's rows once, four rows per step (fewer for wide rows), the first step
+// requested together with the Nexus row: each thread holds 8-element chunks
 // of the rows, the dot products and squared norms are reduced across the
 // workgroup in a fixed order (reproducible), and since a cosine lies in
 // [-1, 1] the softmax needs no running maximum: the weighted sum, the
@@ -19,6 +20,8 @@
 // accumulate in one pass.
 #include "common.h"
 #include "scan.h"
+
+#include <type_traits>
 
 namespace sonic {
 
@@ -97,7 +100,7 @@ __global__ __launch_bounds__(256) void recon_items_kernel(const int32_t *__restr
 // Sum R values over the workgroup, the same order every time; two LDS buffers in turn,
 // so one barrier per call suffices.
 template <int R>
-__device__ __forceinline__ void block_sum(float (&v)[R], float (*red)[kReconWaves][2 * kReconMaxRows], int &par) {
+__device__ __forceinline__ void block_sum(float (&v)[R], float (*red)[kReconWaves][2 * kReconMaxRows + 1], int &par) {
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
 #pragma unroll
   for (int k = 0; k < R; ++k) {
@@ -135,7 +138,7 @@ __global__ __launch_bounds__(kReconThreads) void recon_kernel(const uint16_t *__
                                                               float *__restrict__ cos_out,
                                                               float *__restrict__ ratio_out) {
   static_assert(RW <= kReconMaxRows, "reduction buffer size");
-  __shared__ float red[2][kReconWaves][2 * kReconMaxRows];
+  __shared__ float red[2][kReconWaves][2 * kReconMaxRows + 1];
   const int n_items = ws.ctrl[0];
   const int nch = Dm / 8;
   int par = 0;
@@ -143,30 +146,28 @@ __global__ __launch_bounds__(kReconThreads) void recon_kernel(const uint16_t *__
     const int4 it = items[item];
     const int s = it.y, e = it.z;
     float hn[CPT][8];
-    float nn[1] = {0.f};
+    u32x4 hraw[CPT];
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int c = threadIdx.x + i * kReconThreads;
-      u32x4 w = {0u, 0u, 0u, 0u};
-      if (c < nch) w = *reinterpret_cast<const u32x4 *>(h + static_cast<size_t>(it.x) * Dm + 8 * c);
-      widen8(w, hn[i]);
-#pragma unroll
-      for (int k = 0; k < 8; ++k) nn[0] = fmaf(hn[i][k], hn[i][k], nn[0]);
+      hraw[i] = u32x4{0u, 0u, 0u, 0u};
+      if (c < nch) hraw[i] = *reinterpret_cast<const u32x4 *>(h + static_cast<size_t>(it.x) * Dm + 8 * c);
     }
-    block_sum<1>(nn, red, par);
     float acc[CPT][8];
 #pragma unroll
     for (int i = 0; i < CPT; ++i)
 #pragma unroll
       for (int k = 0; k < 8; ++k) acc[i][k] = 0.f;
-    float Z = 0.f, S1 = 0.f;
-    for (int x0 = s; x0 < e; x0 += RW) {
+    float Z = 0.f, S1 = 0.f, nn = 0.f;
+    // One step: RW rows from x0.  The first step (an interval has at least one row)
+    // requests its rows before the Nexus row is used, so both arrive in one round
+    // trip, and it also reduces |h(N)|^2.
+    auto step = [&](int x0, auto first_tag) {
+      constexpr bool kFirst = decltype(first_tag)::value;
       u32x4 raw[RW][CPT];
-      float dq[2 * RW];   // dot with h(N), then squared norm, per row
+      float dq[kFirst ? 2 * RW + 1 : 2 * RW];   // dot with h(N), then squared norm, per row; |h(N)|^2 last
 #pragma unroll
       for (int r = 0; r < RW; ++r) {
-        dq[r] = 0.f;
-        dq[RW + r] = 0.f;
         const bool ok = x0 + r < e;
 #pragma unroll
         for (int i = 0; i < CPT; ++i) {
@@ -175,8 +176,19 @@ __global__ __launch_bounds__(kReconThreads) void recon_kernel(const uint16_t *__
           if (ok && c < nch) raw[r][i] = *reinterpret_cast<const u32x4 *>(h + static_cast<size_t>(x0 + r) * Dm + 8 * c);
         }
       }
+      if constexpr (kFirst) {
+        dq[2 * RW] = 0.f;
 #pragma unroll
-      for (int r = 0; r < RW; ++r)
+        for (int i = 0; i < CPT; ++i) {
+          widen8(hraw[i], hn[i]);
+#pragma unroll
+          for (int k = 0; k < 8; ++k) dq[2 * RW] = fmaf(hn[i][k], hn[i][k], dq[2 * RW]);
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < RW; ++r) {
+        dq[r] = 0.f;
+        dq[RW + r] = 0.f;
 #pragma unroll
         for (int i = 0; i < CPT; ++i) {
           float f[8];
@@ -187,11 +199,18 @@ __global__ __launch_bounds__(kReconThreads) void recon_kernel(const uint16_t *__
             dq[RW + r] = fmaf(f[k], f[k], dq[RW + r]);
           }
         }
-      block_sum<2 * RW>(dq, red, par);
+      }
+      block_sum(dq, red, par);
+      if constexpr (kFirst) nn = dq[2 * RW];
+      // widen the rows again below rather than keep their fp32 copies live
+#pragma unroll
+      for (int r = 0; r < RW; ++r)
+#pragma unroll
+        for (int i = 0; i < CPT; ++i) asm volatile("" : "+v"(raw[r][i]));
 #pragma unroll
       for (int r = 0; r < RW; ++r) {
         if (x0 + r < e) {
-          const float den = nn[0] * dq[RW + r];
+          const float den = nn * dq[RW + r];
           const float c = den > 0.f ? dq[r] / sqrtf(den) : 0.f;
           const float wgt = expf(c);
           Z += wgt;
@@ -205,7 +224,9 @@ __global__ __launch_bounds__(kReconThreads) void recon_kernel(const uint16_t *__
           }
         }
       }
-    }
+    };
+    step(s, std::true_type{});
+    for (int x0 = s + RW; x0 < e; x0 += RW) step(x0, std::false_type{});
     const float invz = 1.f / Z;
     float tt[2] = {0.f, 0.f};   // target . h(N), |target|^2
 #pragma unroll
@@ -225,7 +246,7 @@ __global__ __launch_bounds__(kReconThreads) void recon_kernel(const uint16_t *__
     }
     block_sum<2>(tt, red, par);
     if (threadIdx.x == 0) {
-      const float den = nn[0] * tt[1];
+      const float den = nn * tt[1];
       cos_out[item] = den > 0.f ? tt[0] / sqrtf(den) : 0.f;
       const int n = e - s;
       ratio_out[item] = n > 1 ? (logf(Z) - S1 * invz) / logf(static_cast<float>(n)) : 1.f;
