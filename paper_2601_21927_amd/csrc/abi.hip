@@ -12,7 +12,7 @@ namespace sonic {
 hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int nexus_scope, const int32_t *cu,
                        const uint8_t *role, const int32_t *turn, const uint16_t *k, const uint16_t *v, PrefillWs ws,
                        int32_t *status, hipStream_t stream);
-hipError_t prefill_occupancy(int D, int G, bool stats, int *blocks);
+hipError_t prefill_occupancy(int D, int G, bool stats, int ks, int *blocks);
 hipError_t launch_recon(int batch, int total_tokens, int Dm, int max_rows, int num_cus, const int32_t *cu,
                         const uint8_t *role, const int32_t *turn, const uint16_t *h, PrefillWs ws,
                         int32_t *nexus_off, int4 *items, float *target, float *cos_out, float *ratio_out,
@@ -30,7 +30,7 @@ hipError_t launch_extend_append(int batch, int max_new, int Hkv, int D, const in
                                 const int32_t *keep_len, uint16_t *kc, uint16_t *vc, const int64_t *row_off,
                                 int32_t *cache_len, const uint16_t *k_new, const uint16_t *v_new,
                                 const int32_t *status, hipStream_t stream);
-hipError_t launch_prefill(int D, int G, int grid, bool stats, AttnRows rows, PrefillWs ws, int Hkv, float scale_log2,
+hipError_t launch_prefill(int D, int G, int grid, bool stats, int ks, AttnRows rows, PrefillWs ws, int Hkv, float scale_log2,
                           hipStream_t stream);
 hipError_t launch_compact(int batch, int total_tokens, int max_seqlen, int Hkv, int D, const int32_t *cu,
                           const uint8_t *role,
@@ -65,6 +65,7 @@ struct DeviceInfo {
   bool valid = false;
   int num_cus = 0;
   int prefill_blocks[2][2][9] = {};   // [statistics variant][D == 128][G]: resident workgroups per CU
+  int prefill_ks2_blocks[2][9] = {};  // the same for the key-split variant, [D == 128][G <= 4]
 };
 
 std::mutex g_dev_mutex;
@@ -84,9 +85,14 @@ hipError_t device_info(DeviceInfo **out) {
       for (int di = 0; di < 2; ++di)
         for (int G = 1; G <= 8; ++G) {
           int blocks = 0;
-          e = prefill_occupancy(di ? 128 : 64, G, st != 0, &blocks);
+          e = prefill_occupancy(di ? 128 : 64, G, st != 0, 1, &blocks);
           if (e != hipSuccess) return e;
           d.prefill_blocks[st][di][G] = blocks > 0 ? blocks : 1;
+          if (st == 0 && G <= 4) {
+            e = prefill_occupancy(di ? 128 : 64, G, false, 2, &blocks);
+            if (e != hipSuccess) return e;
+            d.prefill_ks2_blocks[di][G] = blocks > 0 ? blocks : 1;
+          }
         }
     d.valid = true;
   }
@@ -296,7 +302,7 @@ int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t 
   AttnRows rows{cu_seqlens, nullptr, static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k),
                 static_cast<const uint16_t *>(v), ws.k_pre, ws.v_pre, out, nexus_mass, ws.lse};
   const float scale_log2 = static_cast<float>(softmax_scale * kLog2e);
-  e = launch_prefill(d, G, grid, stats, rows, ws, Hkv, scale_log2, stream);
+  e = launch_prefill(d, G, grid, stats, 1, rows, ws, Hkv, scale_log2, stream);
   if (e == hipSuccess && key_weight != nullptr)
     e = launch_key_weight(batch, total_tokens, Hq, Hkv, d, di->num_cus, cu_seqlens, role,
                           static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k), ws, scale_log2,
@@ -369,12 +375,17 @@ int32_t sonic_nexus_extend(int32_t batch, int32_t total_new, int32_t Hq, int32_t
                          stream);
   if (e != hipSuccess) return SONIC_ERR_HIP;
   if (total_new > 0) {
-    int grid = di->num_cus * di->prefill_blocks[0][d == 128][G];
+    // Fewer work items than twice the CUs (the usual next turn: a few blocks of new
+    // rows per request) would leave CUs idle: split each item's keys over two wave
+    // groups of one workgroup instead.
+    const int64_t item_bound = (static_cast<int64_t>(total_new + kTileRows - 1) / kTileRows + batch) * Hkv;
+    const int ks = (G <= 4 && item_bound <= 2 * static_cast<int64_t>(di->num_cus)) ? 2 : 1;
+    int grid = di->num_cus * (ks == 2 ? di->prefill_ks2_blocks[d == 128][G] : di->prefill_blocks[0][d == 128][G]);
     grid = (grid + kNumXcd - 1) / kNumXcd * kNumXcd;
     AttnRows rows{nexus_cu, cache_row_off, static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k),
                   static_cast<const uint16_t *>(v), static_cast<const uint16_t *>(k_cache),
                   static_cast<const uint16_t *>(v_cache), out};
-    e = launch_prefill(d, G, grid, false, rows, ws, Hkv, static_cast<float>(softmax_scale * kLog2e), stream);
+    e = launch_prefill(d, G, grid, false, ks, rows, ws, Hkv, static_cast<float>(softmax_scale * kLog2e), stream);
     if (e != hipSuccess) return SONIC_ERR_HIP;
   }
   e = launch_extend_append(batch, total_new, Hkv, d, nexus_cu, keep_len, static_cast<uint16_t *>(k_cache),

@@ -147,9 +147,17 @@ __device__ __forceinline__ void stage_tensor(uint16_t *lds_buf, const char *pre_
 // STATS: also write, per row and q-head, the attention mass on the request's
 // Nexus keys (prefix keys at or past its system rows) and the log2-domain softmax
 // normaliser, for the key-weight pass.
-template <int D, int G, bool STATS>
-__global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, PrefillWs ws, int Hkv,
-                                                               float scale_log2) {
+// KS = 2 (G <= 4; for launches with fewer work items than twice the CUs, such as
+// the next-turn Nexus step): the workgroup holds two groups of G waves that take the
+// first and the second half of the item's key steps, each with its own LDS
+// buffers, in lock step (the same number of steps; a step past the end of the
+// list is fully masked).  The second group then hands its (max, sum, O) to the
+// first through LDS, which merges them by log-sum-exp and stores the rows: one
+// resident workgroup per CU with twice the waves, instead of half the CUs idle.
+template <int D, int G, bool STATS, int KS>
+__global__ __launch_bounds__(G * kWave * KS, 3 - KS) void prefill_kernel(AttnRows rows, PrefillWs ws, int Hkv,
+                                                                        float scale_log2) {
+  static_assert(KS == 1 || (KS == 2 && !STATS), "the key split serves the attention output only");
   const uint16_t *__restrict__ q = rows.q;
   float *__restrict__ out = rows.out;
   constexpr int DC = D / 8;              // 16-byte chunks per K/V row
@@ -159,14 +167,26 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, Pr
   // Two buffers per tensor, as distinct arrays: the compiler then knows that the
   // direct-to-LDS loads into one buffer cannot alias reads of the other and does
   // not wait for them before those reads.
-  __shared__ __align__(16) uint16_t k_lds0[kKeyChunk * D];   // [64 keys][D], MFMA row order
-  __shared__ __align__(16) uint16_t k_lds1[kKeyChunk * D];
-  __shared__ __align__(16) uint16_t v_lds0[kKeyChunk * D];   // [64 keys][D], key order
-  __shared__ __align__(16) uint16_t v_lds1[kKeyChunk * D];
+  __shared__ __align__(16) uint16_t k_lds0[KS][kKeyChunk * D];   // [64 keys][D], MFMA row order
+  __shared__ __align__(16) uint16_t k_lds1[KS][kKeyChunk * D];
+  __shared__ __align__(16) uint16_t v_lds0[KS][kKeyChunk * D];   // [64 keys][D], key order
+  __shared__ __align__(16) uint16_t v_lds1[KS][kKeyChunk * D];
+  // KS = 2: the second group's running max and sum per wave and lane (its O goes
+  // to the K/V buffers, one buffer of 64 x D bf16 = 32 x D floats per wave)
+  __shared__ float ml_lds[KS == 2 ? 2 * G * kWave : 1];
+  // KS = 2 keeps two waves per SIMD (G <= 4), so the registers of the single-group
+  // variant still fit; each of the first eight buffers holds one wave's O
+  static_assert(KS == 1 || (G <= 4 && (D / 32) * 16 * kWave <= kKeyChunk * D / 2), "key split shape");
   __shared__ int s_item;
 
   const int Hq = Hkv * G;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);   // uniform: lets waves branch on it
+  const int wave_id = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);   // uniform: lets waves branch on it
+  const int grp = wave_id / G;     // key half (KS = 2)
+  const int wave = wave_id % G;    // q-head within the kv-head's group
+  uint16_t *const kbuf0 = k_lds0[grp];
+  uint16_t *const kbuf1 = k_lds1[grp];
+  uint16_t *const vbuf0 = v_lds0[grp];
+  uint16_t *const vbuf1 = v_lds1[grp];
   const int lane = threadIdx.x % kWave;
   const int n = lane & 31;
   const int g = lane >> 5;
@@ -216,11 +236,20 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, Pr
     const char *kpre = uniform_ptr(reinterpret_cast<const char *>(rows.pre_k + phead0));
     const char *vpre = uniform_ptr(reinterpret_cast<const char *>(rows.pre_v + phead0));
 
+    const int nchunks = (nv + kKeyChunk - 1) / kKeyChunk;
+    // this group's steps: [c_first, c_first + nloc); loads for steps past them
+    // (the pipeline runs two ahead) fetch a step past the list end instead
+    const int nloc = KS == 1 ? nchunks : (nchunks + 1) / 2;
+    const int c_first = grp * nloc;
+    const int c_stop = c_first + nloc;
+    auto stage_step = [&](int c) { return c < c_stop ? c : max(c, nchunks); };
     auto stage_k = [&](int c, uint16_t *buf) {
-      stage_tensor<D, G, false>(buf, kpre, kreq, row_bytes, koff_lane, wave, lane, c, nv, npre, seg_shift);
+      stage_tensor<D, G, false>(buf, kpre, kreq, row_bytes, koff_lane, wave, lane, stage_step(c), nv, npre,
+                                seg_shift);
     };
     auto stage_v = [&](int c, uint16_t *buf) {
-      stage_tensor<D, G, true>(buf, vpre, vreq, row_bytes, voff_lane, wave, lane, c, nv, npre, seg_shift);
+      stage_tensor<D, G, true>(buf, vpre, vreq, row_bytes, voff_lane, wave, lane, stage_step(c), nv, npre,
+                               seg_shift);
     };
 
     // Q^T fragments (B operand of S): lane (row n, half g) holds d = 16*ds + 8*g .. +7.
@@ -245,7 +274,6 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, Pr
     // STATS: Nexus keys are the virtual keys [nex_lo, npre) (the prefix past the system rows)
     const int nex_lo = STATS ? min(ws.req[t.req].system, npre) : npre;
 
-    const int nchunks = (nv + kKeyChunk - 1) / kKeyChunk;
     // One 64-key step: compute on (kc_lds, vc_lds) while step c + 1 streams into
     // (kn_lds, vn_lds).
     // Pipeline, per wave: K of step c + 2 is requested as soon as every wave has
@@ -357,14 +385,51 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, Pr
       }
     };
 
-    stage_k(0, k_lds0);
-    stage_v(0, v_lds0);
-    stage_k(1, k_lds1);
-    step(0, k_lds0, v_lds0, v_lds1);
-    for (int c = 1; c < nchunks; c += 2) {
-      step(c, k_lds1, v_lds1, v_lds0);
-      if (c + 1 >= nchunks) break;
-      step(c + 1, k_lds0, v_lds0, v_lds1);
+    stage_k(c_first, kbuf0);
+    stage_v(c_first, vbuf0);
+    stage_k(c_first + 1, kbuf1);
+    step(c_first, kbuf0, vbuf0, vbuf1);
+    for (int c = 1; c < nloc; c += 2) {
+      step(c_first + c, kbuf1, vbuf1, vbuf0);
+      if (c + 1 >= nloc) break;
+      step(c_first + c + 1, kbuf0, vbuf0, vbuf1);
+    }
+
+    if constexpr (KS == 2) {
+      // the second group hands its partial to the first: wave w's O into buffer w
+      // (lane-minor, so both sides touch consecutive words), max and sum into ml_lds
+      wait_vm<0>();
+      __syncthreads();                 // every wave past its last step's LDS reads and loads
+      uint16_t *const ob = wave < 4 ? (wave < 2 ? k_lds0[wave & 1] : k_lds1[wave & 1])
+                                    : (wave < 6 ? v_lds0[wave & 1] : v_lds1[wave & 1]);
+      float *const xo = reinterpret_cast<float *>(ob);
+      if (grp == 1) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) xo[(db * 16 + e) * kWave + lane] = oacc[db][e];
+        ml_lds[(2 * wave) * kWave + lane] = m_run;
+        ml_lds[(2 * wave + 1) * kWave + lane] = l_run;
+      }
+      __syncthreads();
+      if (grp == 1) continue;          // the loop head's barrier waits for the first group
+      const float m1 = ml_lds[(2 * wave) * kWave + lane];
+      const float l1 = ml_lds[(2 * wave + 1) * kWave + lane];
+      // A group that saw no key of this row (its steps were past the list end) kept
+      // the max at -inf, and its sum and O are NaN (-inf - -inf in the exponent):
+      // select them away rather than scale them by zero.
+      const bool has0 = m_run != -INFINITY, has1 = m1 != -INFINITY;
+      const float mm = fmaxf(m_run, m1);
+      const float c0 = has0 ? __builtin_amdgcn_exp2f(m_run - mm) : 0.f;
+      const float c1 = has1 ? __builtin_amdgcn_exp2f(m1 - mm) : 0.f;
+      l_run = (has0 ? l_run * c0 : 0.f) + (has1 ? l1 * c1 : 0.f);
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float x = xo[(db * 16 + e) * kWave + lane];
+          oacc[db][e] = (has0 ? oacc[db][e] * c0 : 0.f) + (has1 ? x * c1 : 0.f);
+        }
     }
 
     // ---- normalise and store: lane (n, g) holds d = 32*db + 8*i + 4*g + (0..3) ----
@@ -394,19 +459,31 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_kernel(AttnRows rows, Pr
 }
 
 template <int D, int G>
-static hipError_t launch_prefill_dg(int grid, bool stats, AttnRows rows, PrefillWs ws, int Hkv, float scale_log2,
-                                    hipStream_t stream) {
+static hipError_t launch_prefill_dg(int grid, bool stats, int ks, AttnRows rows, PrefillWs ws, int Hkv,
+                                    float scale_log2, hipStream_t stream) {
   if (stats)
-    prefill_kernel<D, G, true><<<dim3(grid), dim3(G * kWave), 0, stream>>>(rows, ws, Hkv, scale_log2);
-  else
-    prefill_kernel<D, G, false><<<dim3(grid), dim3(G * kWave), 0, stream>>>(rows, ws, Hkv, scale_log2);
+    prefill_kernel<D, G, true, 1><<<dim3(grid), dim3(G * kWave), 0, stream>>>(rows, ws, Hkv, scale_log2);
+  else if (ks == 2) {
+    if constexpr (G <= 4)
+      prefill_kernel<D, G, false, 2><<<dim3(grid), dim3(2 * G * kWave), 0, stream>>>(rows, ws, Hkv, scale_log2);
+    else
+      return hipErrorInvalidValue;
+  } else
+    prefill_kernel<D, G, false, 1><<<dim3(grid), dim3(G * kWave), 0, stream>>>(rows, ws, Hkv, scale_log2);
   return hipGetLastError();
 }
 
 template <int D, int G>
-static hipError_t occupancy_dg(bool stats, int *blocks) {
-  if (stats) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, prefill_kernel<D, G, true>, G * kWave, 0);
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, prefill_kernel<D, G, false>, G * kWave, 0);
+static hipError_t occupancy_dg(bool stats, int ks, int *blocks) {
+  if (stats)
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, prefill_kernel<D, G, true, 1>, G * kWave, 0);
+  if (ks == 2) {
+    if constexpr (G <= 4)
+      return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, prefill_kernel<D, G, false, 2>, 2 * G * kWave, 0);
+    else
+      return hipErrorInvalidValue;
+  }
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, prefill_kernel<D, G, false, 1>, G * kWave, 0);
 }
 
 #define SONIC_FOR_G(D, X) \
@@ -422,8 +499,8 @@ static hipError_t occupancy_dg(bool stats, int *blocks) {
     default: return hipErrorInvalidValue; \
   }
 
-hipError_t prefill_occupancy(int D, int G, bool stats, int *blocks) {
-#define OCC(DD, GG) return occupancy_dg<DD, GG>(stats, blocks)
+hipError_t prefill_occupancy(int D, int G, bool stats, int ks, int *blocks) {
+#define OCC(DD, GG) return occupancy_dg<DD, GG>(stats, ks, blocks)
   if (D == 64) {
     SONIC_FOR_G(64, OCC)
   } else if (D == 128) {
@@ -433,9 +510,9 @@ hipError_t prefill_occupancy(int D, int G, bool stats, int *blocks) {
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_prefill(int D, int G, int grid, bool stats, AttnRows rows, PrefillWs ws, int Hkv,
+hipError_t launch_prefill(int D, int G, int grid, bool stats, int ks, AttnRows rows, PrefillWs ws, int Hkv,
                           float scale_log2, hipStream_t stream) {
-#define LAUNCH(DD, GG) return launch_prefill_dg<DD, GG>(grid, stats, rows, ws, Hkv, scale_log2, stream)
+#define LAUNCH(DD, GG) return launch_prefill_dg<DD, GG>(grid, stats, ks, rows, ws, Hkv, scale_log2, stream)
   if (D == 64) {
     SONIC_FOR_G(64, LAUNCH)
   } else if (D == 128) {

@@ -211,3 +211,13 @@ def test_extend_argument_errors():
         sonic.nexus_extend(case.nexus_cu, case.keep_len.long(), case.kc, case.vc, case.row_off, case.row_cap,
                            case.length, case.q, case.k, case.v, case.out, case.ws, case.status,
                            max_rows=int(case.cap.max()))
+
+
+def test_extend_many_new_rows():
+    """Enough new rows that the work items outnumber twice the CUs (one wave group per
+    item, no key split), with ragged blocks: 4 requests, 2,396 new Nexus rows."""
+    H.need_gpu()
+    lays = [W.RequestLayout(40, [100, 700], [20, 600], 0), W.RequestLayout(3, [650], [599], 0),
+            W.RequestLayout(17, [30, 612], [5, 598], 0), W.RequestLayout(0, [720], [599], 0)]
+    batch = W.make_batch("ext-many", lays, 32, 8, 128, seed=21)
+    check_case(ExtendCase(batch), "many rows")
