@@ -15,7 +15,7 @@ hipError_t launch_plan(int batch, int total_tokens, int Hkv, int D, int nexus_sc
 hipError_t prefill_occupancy(int D, int G, bool stats, int ks, int *blocks);
 hipError_t launch_recon(int batch, int total_tokens, int Dm, int max_rows, int num_cus, const int32_t *cu,
                         const uint8_t *role, const int32_t *turn, const uint16_t *h, PrefillWs ws,
-                        int32_t *nexus_off, int4 *items, float *target, float *cos_out, float *ratio_out,
+                        int4 *items, float *target, float *cos_out, float *ratio_out,
                         int32_t *status, hipStream_t stream);
 hipError_t launch_routed_gemm(int T, int K, int N, const uint8_t *role, const uint16_t *x, const uint16_t *w_text,
                               const uint16_t *w_nexus, float *y, int32_t *blk_nexus, int32_t *counts, int32_t *perm,
@@ -439,8 +439,7 @@ int32_t sonic_role_projection(int32_t T, int32_t K, int32_t N, const uint8_t *ro
 }
 
 // ---------------------------------------------------------------- reconstruction targets
-static size_t recon_ws_layout(int32_t batch, int32_t T, PrefillWs *ws, int32_t **nexus_off, int4 **items,
-                              char *base) {
+static size_t recon_ws_layout(int32_t batch, int32_t T, PrefillWs *ws, int4 **items, char *base) {
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -454,7 +453,6 @@ static size_t recon_ws_layout(int32_t batch, int32_t T, PrefillWs *ws, int32_t *
   char *runs = take(sizeof(int2) * T1);
   char *tiles = take(sizeof(TileDesc) * T1);
   char *ctrl = take(sizeof(int32_t) * 16);
-  char *noff = take(sizeof(int32_t) * B1);
   char *it = take(sizeof(int4) * T1);
   if (ws) {
     *ws = PrefillWs{};
@@ -463,7 +461,6 @@ static size_t recon_ws_layout(int32_t batch, int32_t T, PrefillWs *ws, int32_t *
     ws->runs = reinterpret_cast<int2 *>(runs);
     ws->tiles = reinterpret_cast<TileDesc *>(tiles);
     ws->ctrl = reinterpret_cast<int32_t *>(ctrl);
-    *nexus_off = reinterpret_cast<int32_t *>(noff);
     *items = reinterpret_cast<int4 *>(it);
   }
   return off;
@@ -471,7 +468,7 @@ static size_t recon_ws_layout(int32_t batch, int32_t T, PrefillWs *ws, int32_t *
 
 size_t sonic_nexus_recon_workspace_bytes(int32_t batch, int32_t total_tokens) {
   if (batch < 0 || total_tokens < 0) return 0;
-  return recon_ws_layout(batch, total_tokens, nullptr, nullptr, nullptr, nullptr);
+  return recon_ws_layout(batch, total_tokens, nullptr, nullptr, nullptr);
 }
 
 int32_t sonic_nexus_recon_targets(int32_t batch, int32_t T, int32_t Dm, const int32_t *cu_seqlens,
@@ -488,15 +485,14 @@ int32_t sonic_nexus_recon_targets(int32_t batch, int32_t T, int32_t Dm, const in
     return SONIC_ERR_INVALID_ARG;
   if (!aligned(h, 16) || !aligned(target, 16) || !aligned(workspace, 256)) return SONIC_ERR_INVALID_ARG;
   PrefillWs ws;
-  int32_t *nexus_off = nullptr;
   int4 *items = nullptr;
-  if (workspace_bytes < recon_ws_layout(batch, T, &ws, &nexus_off, &items, static_cast<char *>(workspace)))
+  if (workspace_bytes < recon_ws_layout(batch, T, &ws, &items, static_cast<char *>(workspace)))
     return SONIC_ERR_WORKSPACE;
   DeviceInfo *di = nullptr;
   hipError_t e = device_info(&di);
   if (e != hipSuccess) return SONIC_ERR_HIP;
   e = launch_recon(batch, T, Dm, max_rows, di->num_cus, cu_seqlens, role, turn_id, static_cast<const uint16_t *>(h),
-                   ws, nexus_off, items, target, cos_target, entropy_ratio, dev_status, stream);
+                   ws, items, target, cos_target, entropy_ratio, dev_status, stream);
   return finish(e, dev_status, stream);
 }
 

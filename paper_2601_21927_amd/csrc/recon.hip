@@ -8,8 +8,8 @@
 // (1 for a one-token interval).  A zero vector has cosine 0 with anything.
 //
 // The segment structure comes from the prefill planner's run table; one small
-// kernel numbers the Nexus tokens of the batch (position order) and one lists,
-// per Nexus token, its position and its interval.  The pooling is HBM-bound:
+// kernel numbers the Nexus tokens of the batch (position order) and lists, per
+// Nexus token, its position and its interval.  The pooling is HBM-bound:
 // one workgroup per Nexus token (persistent grid) reads the Nexus row and its
 // interval's rows once, four rows per step (fewer for wide rows), the first step
 // requested together with the Nexus row: each thread holds 8-element chunks
@@ -32,45 +32,55 @@ constexpr int kReconMaxRows = 4;   // body rows per step (fewer for wide rows)
 hipError_t launch_plan_runs(int batch, int total_tokens, const int32_t *cu, const uint8_t *role, const int32_t *turn,
                             PrefillWs ws, int32_t *status, hipStream_t stream);
 
-// One workgroup: first output row of each request's Nexus tokens; ctrl[0] = their total
-// (0 when it exceeds the caller's rows, which is reported).
-__global__ __launch_bounds__(1024) void recon_offsets_kernel(int batch, int max_rows, PrefillWs ws,
-                                                             int32_t *__restrict__ nexus_off, int32_t *status) {
-  __shared__ int lds[1024 / kWave + 1];
-  __shared__ int s_ok;
-  const bool ok = block_status_clear(status, &s_ok);
-  int carry = 0;
-  for (int base = 0; base < batch; base += 1024) {
-    const int b = base + threadIdx.x;
-    const int v = (ok && b < batch) ? ws.req[b].nexus_total : 0;
-    int tot;
-    const int off = block_int_scan<1024>(v, &tot, lds);
-    if (b < batch) nexus_off[b] = carry + off;
-    carry += tot;
-  }
-  if (threadIdx.x == 0) {
-    const bool fits = carry <= max_rows;
-    if (ok && !fits) raise_status(status, SONIC_ERR_CAPACITY);
-    ws.ctrl[0] = (ok && fits) ? carry : 0;
-  }
-}
-
 // Per request: one item per Nexus token, (position, first interval row, end row), rows
-// as batch positions.  The run table is read 256 runs at a time into LDS; then the
-// workgroup walks those runs and its threads fill a Nexus run's items in parallel.
-__global__ __launch_bounds__(256) void recon_items_kernel(const int32_t *__restrict__ cu,
+// as batch positions.  The workgroup first sums the Nexus counts of the requests
+// before its own (its first output row) and of the whole batch; workgroup 0 stores
+// the total in ctrl[0] (0 when it exceeds the caller's rows, which it reports), and
+// nothing is listed then.  The run table is read 256 runs at a time into LDS; then
+// the workgroup walks those runs and its threads fill a Nexus run's items in parallel.
+__global__ __launch_bounds__(256) void recon_items_kernel(int batch, int max_rows, const int32_t *__restrict__ cu,
                                                           const uint8_t *__restrict__ role, PrefillWs ws,
-                                                          const int32_t *__restrict__ nexus_off,
-                                                          int4 *__restrict__ items) {
+                                                          int4 *__restrict__ items, int32_t *status) {
   __shared__ int s_x[256 + 2];    // starts of runs c0 - 1 .. c0 + 256 (the last: the next run or L)
   __shared__ int s_y[256];        // prefix rows (system + Nexus) before each run
   __shared__ int s_nx[256];       // run is a Nexus run
-  if (ws.ctrl[0] == 0) return;
+  __shared__ int s_red[2][256 / kWave];
+  __shared__ int s_ok;
+  const bool clear = block_status_clear(status, &s_ok);
   const int b = blockIdx.x;
+  int before = 0, total = 0;
+  for (int i = threadIdx.x; i < batch; i += 256) {
+    const int n = ws.req[i].nexus_total;
+    total += n;
+    before += i < b ? n : 0;
+  }
+#pragma unroll
+  for (int o = kWave / 2; o > 0; o >>= 1) {
+    total += __shfl_xor(total, o);
+    before += __shfl_xor(before, o);
+  }
+  if (threadIdx.x % kWave == 0) {
+    s_red[0][threadIdx.x / kWave] = total;
+    s_red[1][threadIdx.x / kWave] = before;
+  }
+  __syncthreads();
+  total = 0;
+  before = 0;
+#pragma unroll
+  for (int w = 0; w < 256 / kWave; ++w) {
+    total += s_red[0][w];
+    before += s_red[1][w];
+  }
+  const bool fits = total <= max_rows;
+  if (b == 0 && threadIdx.x == 0) {
+    if (clear && !fits) raise_status(status, SONIC_ERR_CAPACITY);
+    ws.ctrl[0] = (clear && fits) ? total : 0;
+  }
+  if (!clear || !fits) return;
   const int s0 = cu[b];
   const int L = cu[b + 1] - s0;
   const ReqInfo ri = ws.req[b];
-  const int base = nexus_off[b] - ri.system;
+  const int base = before - ri.system;
   for (int c0 = 0; c0 < ri.nruns; c0 += 256) {
     const int cnt = min(256, ri.nruns - c0);
     if (threadIdx.x < cnt) {
@@ -256,12 +266,11 @@ __global__ __launch_bounds__(kReconThreads) void recon_kernel(const uint16_t *__
 
 hipError_t launch_recon(int batch, int total_tokens, int Dm, int max_rows, int num_cus, const int32_t *cu,
                         const uint8_t *role, const int32_t *turn, const uint16_t *h, PrefillWs ws,
-                        int32_t *nexus_off, int4 *items, float *target, float *cos_out, float *ratio_out,
+                        int4 *items, float *target, float *cos_out, float *ratio_out,
                         int32_t *status, hipStream_t stream) {
   hipError_t e = launch_plan_runs(batch, total_tokens, cu, role, turn, ws, status, stream);
   if (e != hipSuccess) return e;
-  recon_offsets_kernel<<<dim3(1), dim3(1024), 0, stream>>>(batch, max_rows, ws, nexus_off, status);
-  recon_items_kernel<<<dim3(batch), dim3(256), 0, stream>>>(cu, role, ws, nexus_off, items);
+  recon_items_kernel<<<dim3(batch), dim3(256), 0, stream>>>(batch, max_rows, cu, role, ws, items, status);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int chunks = (Dm / 8 + kReconThreads - 1) / kReconThreads;
