@@ -29,6 +29,7 @@
 namespace sonic {
 
 constexpr int kPlanThreads = 1024;
+constexpr int kPlanTok = 8;        // tokens per thread in the run kernel's pass 1
 constexpr int kCostBuckets = 1024;
 
 // One step of the grammar SYSTEM* (TEXT+ NEXUS*)* CURRENT* of Eq.(1): may a token
@@ -64,8 +65,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_runs_kernel(const int32_t *
                                                                  int total_tokens, int nexus_scope,
                                                                  int32_t *status) {
   __shared__ int lds[kPlanThreads / kWave + 1];
-  __shared__ int lds3[3 * (kPlanThreads / kWave)];
-  __shared__ int s_bad;
+  __shared__ int lds4[4 * (kPlanThreads / kWave)];
   __shared__ unsigned long long s_cost;
   const int b = blockIdx.x;
   const int s = cu[b];
@@ -78,54 +78,76 @@ __global__ __launch_bounds__(kPlanThreads) void plan_runs_kernel(const int32_t *
     return;
   }
   const int L = e - s;
-  if (threadIdx.x == 0) s_bad = 0;
-  __syncthreads();
 
   // Pass 1: grammar, prefix rows (system and Nexus positions, in order), run starts
   // with the number of prefix rows before each.  In a well-formed request the
   // system rows come first, so the prefix is the system prompt followed by the
-  // Nexus tokens.
-  // The next 1024 tokens are requested before the current ones are counted, so
-  // their load latency overlaps the scan (whose barriers wait for LDS only).
-  int pre_carry = 0, run_carry = 0, nexus_count = 0;
-  // A token's predecessor comes from the lane below; lane 0 of each wave loads its own.
+  // Nexus tokens.  Each thread takes kPlanTok consecutive tokens (one chunk of
+  // kPlanThreads * kPlanTok tokens covers most requests): it counts them, one
+  // block scan places its entries, and a second walk over its registers writes
+  // them.  A token's predecessor is the thread's previous token, or the lower
+  // lane's last one (lane 0 loads its own).
+  int pre_carry = 0, run_carry = 0, nexus_count = 0, bad_count = 0;
   const int lane = threadIdx.x % kWave;
-  auto fetch = [&](int base, int &r, int &t, int &rp, int &tp) {
-    const int i = base + threadIdx.x;
-    r = -1, t = 0, rp = -1, tp = 0;
-    if (i < L) {
-      r = role[s + i];
-      t = turn[s + i];
-      if (lane == 0 && i > 0) {
-        rp = role[s + i - 1];
-        tp = turn[s + i - 1];
+  for (int base = 0; base < L; base += kPlanThreads * kPlanTok) {
+    const int i0 = base + threadIdx.x * kPlanTok;
+    int r[kPlanTok], t[kPlanTok];
+#pragma unroll
+    for (int j = 0; j < kPlanTok; ++j) {
+      r[j] = -1;
+      t[j] = 0;
+      if (i0 + j < L) {
+        r[j] = role[s + i0 + j];
+        t[j] = turn[s + i0 + j];
       }
     }
-  };
-  int nr, nt, nrp, ntp;
-  fetch(0, nr, nt, nrp, ntp);
-  for (int base = 0; base < L; base += kPlanThreads) {
-    const int i = base + threadIdx.x;
-    const bool in = i < L;
-    const int r = nr, t = nt;
-    const int up_r = __shfl_up(r, 1), up_t = __shfl_up(t, 1);
-    const int rp = lane == 0 ? nrp : (i > 0 ? up_r : -1);
-    const int tp = lane == 0 ? ntp : (i > 0 ? up_t : 0);
-    if (base + kPlanThreads < L) fetch(base + kPlanThreads, nr, nt, nrp, ntp);
-    if (in && !legal_step(rp, tp, r, t)) s_bad = 1;
-    const bool is_pre = in && (r == kSystem || r == kNexus);
-    const bool run_start = in && (i == 0 || r != rp || (r == kText && t != tp));
-    const bool flags[3] = {is_pre, run_start, in && r == kNexus};
-    int below[3], tot[3];
-    block_flags_scan<kPlanThreads, 3>(flags, below, tot, lds3);
-    if (is_pre) ws.prefix_pos[s + pre_carry + below[0]] = i;
-    if (run_start) ws.runs[s + run_carry + below[1]] = make_int2(i, pre_carry + below[0]);
+    int rp0 = __shfl_up(r[kPlanTok - 1], 1), tp0 = __shfl_up(t[kPlanTok - 1], 1);
+    if (lane == 0) {
+      rp0 = -1;
+      tp0 = 0;
+      if (i0 > 0 && i0 <= L) {
+        rp0 = role[s + i0 - 1];
+        tp0 = turn[s + i0 - 1];
+      }
+    }
+    int cnt[4] = {0, 0, 0, 0};   // prefix rows, run starts, Nexus tokens, illegal steps
+    {
+      int rp = rp0, tp = tp0;
+#pragma unroll
+      for (int j = 0; j < kPlanTok; ++j) {
+        if (i0 + j < L) {
+          cnt[0] += (r[j] == kSystem || r[j] == kNexus) ? 1 : 0;
+          cnt[1] += (i0 + j == 0 || r[j] != rp || (r[j] == kText && t[j] != tp)) ? 1 : 0;
+          cnt[2] += r[j] == kNexus ? 1 : 0;
+          cnt[3] += legal_step(rp, tp, r[j], t[j]) ? 0 : 1;
+        }
+        rp = r[j];
+        tp = t[j];
+      }
+    }
+    int below[4], tot[4];
+    block_int_scan_n<kPlanThreads, 4>(cnt, below, tot, lds4);
+    {
+      int rp = rp0, tp = tp0;
+      int pc = pre_carry + below[0], rc = run_carry + below[1];
+#pragma unroll
+      for (int j = 0; j < kPlanTok; ++j) {
+        const int i = i0 + j;
+        if (i < L) {
+          if (i == 0 || r[j] != rp || (r[j] == kText && t[j] != tp)) ws.runs[s + rc++] = make_int2(i, pc);
+          if (r[j] == kSystem || r[j] == kNexus) ws.prefix_pos[s + pc++] = i;
+        }
+        rp = r[j];
+        tp = t[j];
+      }
+    }
     pre_carry += tot[0];
     run_carry += tot[1];
     nexus_count += tot[2];
+    bad_count += tot[3];
   }
   __syncthreads();
-  if (s_bad) {
+  if (bad_count) {
     if (threadIdx.x == 0) {
       raise_status(status, SONIC_ERR_BAD_LAYOUT);
       ws.req[b] = ReqInfo{0, 0, 0, 0, 0, 0};

@@ -73,6 +73,44 @@ __device__ __forceinline__ void block_flags_scan(const bool (&flag)[NF], int (&b
   lds_barrier();
 }
 
+// Exclusive prefix sums of NV ints at once over an NT-thread workgroup: below[f] =
+// the sum of x[f] over lower threads, total[f] = the workgroup's sum.  Two barriers.
+template <int NT, int NV>
+__device__ __forceinline__ void block_int_scan_n(const int (&x)[NV], int (&below)[NV], int (&total)[NV],
+                                                 int *lds) {
+  constexpr int NW = NT / kWave;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int w = threadIdx.x / kWave;
+  int v[NV];
+#pragma unroll
+  for (int f = 0; f < NV; ++f) v[f] = x[f];
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+#pragma unroll
+    for (int f = 0; f < NV; ++f) {
+      const int y = __shfl_up(v[f], o);
+      if (lane >= o) v[f] += y;
+    }
+  }
+  if (lane == kWave - 1)
+#pragma unroll
+    for (int f = 0; f < NV; ++f) lds[f * NW + w] = v[f];
+  lds_barrier();
+#pragma unroll
+  for (int f = 0; f < NV; ++f) {
+    int before = 0, tot = 0;
+#pragma unroll
+    for (int k = 0; k < NW; ++k) {
+      const int c = lds[f * NW + k];
+      before += k < w ? c : 0;
+      tot += c;
+    }
+    below[f] = v[f] - x[f] + before;
+    total[f] = tot;
+  }
+  lds_barrier();
+}
+
 // Exclusive prefix sum of a non-negative int over an NT-thread workgroup.
 template <int NT>
 __device__ __forceinline__ int block_int_scan(int x, int *total, int *lds) {
