@@ -181,8 +181,8 @@ __global__ __launch_bounds__(G * kWave * KS, 3 - KS) void prefill_kernel(AttnRow
 
   const int Hq = Hkv * G;
   const int wave_id = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);   // uniform: lets waves branch on it
-  const int grp = wave_id / G;     // key half (KS = 2)
-  const int wave = wave_id % G;    // q-head within the kv-head's group
+  const int grp = KS == 1 ? 0 : wave_id / G;          // key half (KS = 2)
+  const int wave = KS == 1 ? wave_id : wave_id % G;   // q-head within the kv-head's group
   uint16_t *const kbuf0 = k_lds0[grp];
   uint16_t *const kbuf1 = k_lds1[grp];
   uint16_t *const vbuf0 = v_lds0[grp];
@@ -242,7 +242,7 @@ __global__ __launch_bounds__(G * kWave * KS, 3 - KS) void prefill_kernel(AttnRow
     const int nloc = KS == 1 ? nchunks : (nchunks + 1) / 2;
     const int c_first = grp * nloc;
     const int c_stop = c_first + nloc;
-    auto stage_step = [&](int c) { return c < c_stop ? c : max(c, nchunks); };
+    auto stage_step = [&](int c) { return (KS == 1 || c < c_stop) ? c : max(c, nchunks); };
     auto stage_k = [&](int c, uint16_t *buf) {
       stage_tensor<D, G, false>(buf, kpre, kreq, row_bytes, koff_lane, wave, lane, stage_step(c), nv, npre,
                                 seg_shift);
