@@ -38,41 +38,6 @@ __device__ __forceinline__ int block_flag_scan(bool flag, int *total, int *lds) 
   return res;
 }
 
-// Exclusive prefix counts of NF 0/1 flags at once over an NT-thread workgroup:
-// below[f] = threads before this one with flag f set, total[f] = the workgroup's
-// count.  Two barriers for all NF flags; every thread sums the per-wave counts
-// it needs itself (broadcast LDS reads), so no thread walks the waves serially.
-// The barriers wait for LDS only: global loads in flight (a prefetch) stay in
-// flight, and global stores made before the scan are not ordered by it.
-// `lds` must hold NF * NT/64 ints.
-template <int NT, int NF>
-__device__ __forceinline__ void block_flags_scan(const bool (&flag)[NF], int (&below)[NF], int (&total)[NF],
-                                                 int *lds) {
-  constexpr int NW = NT / kWave;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int w = threadIdx.x / kWave;
-#pragma unroll
-  for (int f = 0; f < NF; ++f) {
-    const uint64_t m = __ballot(flag[f]);
-    below[f] = lanes_below(m);
-    if (lane == 0) lds[f * NW + w] = __popcll(m);
-  }
-  lds_barrier();
-#pragma unroll
-  for (int f = 0; f < NF; ++f) {
-    int before = 0, tot = 0;
-#pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      const int c = lds[f * NW + i];
-      before += i < w ? c : 0;
-      tot += c;
-    }
-    below[f] += before;
-    total[f] = tot;
-  }
-  lds_barrier();
-}
-
 // Exclusive prefix sums of NV ints at once over an NT-thread workgroup: below[f] =
 // the sum of x[f] over lower threads, total[f] = the workgroup's sum.  Two barriers.
 template <int NT, int NV>
