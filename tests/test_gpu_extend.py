@@ -103,7 +103,8 @@ def _ending_layouts(rng, n, **kw):
     return out
 
 
-@pytest.mark.parametrize("Hq,Hkv,d", [(4, 2, 64), (32, 8, 128), (28, 4, 128), (8, 1, 64), (6, 2, 128)])
+@pytest.mark.parametrize("Hq,Hkv,d", [(4, 2, 64), (32, 8, 128), (28, 4, 128), (8, 1, 64), (6, 2, 128),
+                                      (2, 2, 128), (3, 1, 64)])
 def test_extend_random(Hq, Hkv, d):
     H.need_gpu()
     rng = np.random.default_rng(300 + Hq + Hkv + d)
