@@ -11,7 +11,7 @@
 // kernel numbers the Nexus tokens of the batch (position order) and lists, per
 // Nexus token, its position and its interval.  The pooling is HBM-bound:
 // one workgroup per Nexus token (persistent grid) reads the Nexus row and its
-// interval's rows once, four rows per step (fewer for wide rows), the first step
+// interval's rows once, four or six rows per step (fewer for wide rows), the first step
 // requested together with the Nexus row: each thread holds 8-element chunks
 // of the rows, the dot products and squared norms are reduced across the
 // workgroup in a fixed order (reproducible), and since a cosine lies in
@@ -27,7 +27,7 @@ namespace sonic {
 
 constexpr int kReconThreads = 256;
 constexpr int kReconWaves = kReconThreads / kWave;
-constexpr int kReconMaxRows = 4;   // body rows per step (fewer for wide rows)
+constexpr int kReconMaxRows = 6;   // body rows per step (fewer for wide rows)
 
 hipError_t launch_plan_runs(int batch, int total_tokens, const int32_t *cu, const uint8_t *role, const int32_t *turn,
                             PrefillWs ws, int32_t *status, hipStream_t stream);
@@ -278,7 +278,7 @@ hipError_t launch_recon(int batch, int total_tokens, int Dm, int max_rows, int n
   if (chunks <= 1)
     recon_kernel<1, 4><<<grid, block, 0, stream>>>(h, Dm, items, ws, target, cos_out, ratio_out);
   else if (chunks <= 2)
-    recon_kernel<2, 4><<<grid, block, 0, stream>>>(h, Dm, items, ws, target, cos_out, ratio_out);
+    recon_kernel<2, 6><<<grid, block, 0, stream>>>(h, Dm, items, ws, target, cos_out, ratio_out);
   else if (chunks <= 4)
     recon_kernel<4, 2><<<grid, block, 0, stream>>>(h, Dm, items, ws, target, cos_out, ratio_out);
   else
