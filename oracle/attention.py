@@ -57,7 +57,12 @@ def request_probs(q, k, role, turn_id, h: int, scale=None, rows=None, nexus_scop
 
 def prefill_request(q, k, v, role, turn_id, scale=None, rows=None, block=512,
                     parsed: Parsed = None, nexus_scope: str = NEXUS_ALL) -> np.ndarray:
-    """O[rows, Hq, d] for one request: dense scores, explicit mask, softmax, P @ V."""
+    """O[rows, Hq, d] for one request: dense scores, explicit mask, softmax, P @ V.
+
+    Per block of query rows the mask is built over every key; key columns that no
+    row of the block sees are then left out of the products.  Their entries of M
+    are -inf (Sec. 3.2), so their probabilities are exactly 0 and the result is
+    the same softmax over the same visible keys."""
     kf = bf16_bits_to_f64(k)
     vf = bf16_bits_to_f64(v)
     L, Hq, d = q.shape
@@ -74,11 +79,13 @@ def prefill_request(q, k, v, role, turn_id, scale=None, rows=None, block=512,
         rb = rows[r0:r0 + block]
         qf = bf16_bits_to_f64(q[rb])          # only the query rows of this block
         vis = visibility_rows(role, turn_id, rb, parsed=parsed, nexus_scope=nexus_scope)
+        cols = np.flatnonzero(vis.any(axis=0))   # keys some row of the block sees
+        vis = vis[:, cols]
         for h in range(Hq):
             g = kv_head(h, Hq, Hkv)
-            scores = scale * (qf[:, h, :] @ kf[:, g, :].T)
+            scores = scale * (qf[:, h, :] @ kf[cols, g, :].T)
             probs = softmax_probs(scores, vis)
-            out[r0:r0 + len(rb), h, :] = probs @ vf[:, g, :]
+            out[r0:r0 + len(rb), h, :] = probs @ vf[cols, g, :]
     return out
 
 
