@@ -38,11 +38,15 @@
  *   tokens; it then ends at its last body token.
  * - Synchronous errors (bad arguments, unsupported shapes, small workspace) are
  *   returned before anything is enqueued; outputs are untouched.
- * - Asynchronous errors (layout grammar, cache capacity) are found by the
- *   kernels and written to the device word *dev_status (first error wins).  The
- *   caller zeroes *dev_status before first use.  While it is non-zero every
- *   later kernel of this library that receives it returns without writing its
- *   outputs, so an error is sticky until the caller clears it.
+ * - Asynchronous errors (layout grammar, cache capacity, a size argument the
+ *   device data contradicts) are found by the kernels and written to the device
+ *   word *dev_status (first error wins).  The caller zeroes *dev_status before
+ *   first use.  While it is non-zero every later kernel of this library that
+ *   receives it returns without writing its outputs, so an error is sticky until
+ *   the caller clears it.  The one exception is a pending SONIC_ERR_CAPACITY in
+ *   sonic_compressed_decode, where capacity is a per-request matter (see there).
+ * - softmax_scale: 0 selects the standard scale 1/sqrt(head_dim); any other value
+ *   must be finite and positive.
  * - Setting the environment variable SONIC_DEBUG_SYNC=1 makes each GPU call
  *   synchronise its stream and return the device status (debugging only).
  * - Thread safety: calls are independent; the library keeps no mutable global
@@ -155,7 +159,7 @@ size_t sonic_prefill_workspace_bytes(int32_t batch, int32_t total_tokens, int32_
  *   cu_seqlens            device int32 [B+1], non-decreasing, cu[0] = 0
  *   role, turn_id         device uint8 [T], int32 [T]
  *   q                     device bf16 [T][Hq][d];  k, v: device bf16 [T][Hkv][d]
- *   softmax_scale         finite and > 0, e.g. 1/sqrt(d)
+ *   softmax_scale         0 for 1/sqrt(d), else finite and > 0
  *   nexus_scope           SONIC_NEXUS_ALL or SONIC_NEXUS_UP_TO_OWN
  *   out                   device fp32 [T][Hq][d] (fully written on success)
  *   nexus_mass            NULL, or device fp32 [T][Hq]: per row p and q-head h the
@@ -265,8 +269,13 @@ int32_t sonic_nexus_recon_targets(int32_t batch, int32_t total_tokens, int32_t h
  * request's capacity are not written.
  *
  *   batch, total_tokens, max_seqlen  host values; max_seqlen >= every request length
+ *                                    (the grid is sized from it: a longer request
+ *                                    raises SONIC_ERR_INVALID_ARG on the device and
+ *                                    none of its rows is written)
  *   num_kv_heads, head_dim           Hkv, d (d in {64, 128})
- *   cu_seqlens, role                 device, as for the prefill
+ *   cu_seqlens, role                 device, as for the prefill; role 16-byte
+ *                                    aligned (it is read in 16-byte words, never
+ *                                    past its total_tokens bytes)
  *   k, v                             device bf16 [T][Hkv][d]
  *   k_cache, v_cache                 device bf16 [rows][Hkv][d]
  *   cache_row_off                    device int64 [B]: first cache row of request b
@@ -315,8 +324,12 @@ size_t sonic_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t 
  *                  counters that every call leaves at zero again)
  *   dev_status     SONIC_ERR_CAPACITY when cache_len[b] + 1 exceeds the capacity
  *                  or max_ctx: request b is then left unchanged (no append, no
- *                  output, same length) while the other requests proceed.  Unlike
- *                  the other calls, decode does not skip work on a pending status.
+ *                  output, same length) while the other requests proceed.
+ *                  Capacity is per request, so a pending SONIC_ERR_CAPACITY does
+ *                  not stop later decode calls either (each full request keeps
+ *                  failing on its own).  Any other pending error (a layout or
+ *                  argument error of an earlier call) stops the call: nothing is
+ *                  appended, written or advanced for any request.
  * Calls that share a workspace must not run concurrently.
  */
 int32_t sonic_compressed_decode(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,

@@ -45,12 +45,15 @@ hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int nsp
 
 namespace {
 
-constexpr int kAbiVersion = 7;
+constexpr int kAbiVersion = 8;
 constexpr double kLog2e = 1.4426950408889634;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// softmax_scale == 0 selects the standard scaled dot-product attention scale 1/sqrt(d)
+float default_scale(float scale, int d) { return scale == 0.f ? static_cast<float>(1.0 / std::sqrt(double(d))) : scale; }
 
 bool debug_sync() {
   static const bool on = [] {
@@ -278,7 +281,8 @@ int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t 
   if (Hq % Hkv != 0) return SONIC_ERR_INVALID_ARG;
   const int G = Hq / Hkv;
   if (G > 8) return SONIC_ERR_UNSUPPORTED;
-  if (!std::isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SONIC_ERR_INVALID_ARG;
+  if (!std::isfinite(softmax_scale) || softmax_scale < 0.f) return SONIC_ERR_INVALID_ARG;
+  softmax_scale = default_scale(softmax_scale, d);
   if (batch == 0 || total_tokens == 0) return SONIC_OK;
   if (!cu_seqlens || !role || !turn_id || !q || !k || !v || !out || !workspace) return SONIC_ERR_INVALID_ARG;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) || !aligned(workspace, 256) ||
@@ -352,7 +356,8 @@ int32_t sonic_nexus_extend(int32_t batch, int32_t total_new, int32_t Hq, int32_t
   const int G = Hq / Hkv;
   if (G > 8) return SONIC_ERR_UNSUPPORTED;
   if (batch > 65535) return SONIC_ERR_UNSUPPORTED;
-  if (!std::isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SONIC_ERR_INVALID_ARG;
+  if (!std::isfinite(softmax_scale) || softmax_scale < 0.f) return SONIC_ERR_INVALID_ARG;
+  softmax_scale = default_scale(softmax_scale, d);
   if (batch == 0) return SONIC_OK;
   if (!nexus_cu || !keep_len || !k_cache || !v_cache || !cache_row_off || !cache_row_cap || !cache_len ||
       !workspace || (total_new > 0 && (!q || !k || !v || !out)))
@@ -545,7 +550,8 @@ int32_t sonic_compressed_decode(int32_t batch, int32_t Hq, int32_t Hkv, int32_t 
   if (Hq % Hkv != 0) return SONIC_ERR_INVALID_ARG;
   if (Hq / Hkv > 8) return SONIC_ERR_UNSUPPORTED;
   if (batch > 65535 || Hkv > 65535) return SONIC_ERR_UNSUPPORTED;
-  if (!std::isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SONIC_ERR_INVALID_ARG;
+  if (!std::isfinite(softmax_scale) || softmax_scale < 0.f) return SONIC_ERR_INVALID_ARG;
+  softmax_scale = default_scale(softmax_scale, d);
   if (batch == 0) return SONIC_OK;
   if (!k_cache || !v_cache || !cache_row_off || !cache_row_cap || !cache_len || !q || !k_new || !v_new || !out ||
       !workspace)

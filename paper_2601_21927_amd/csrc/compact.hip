@@ -3,14 +3,20 @@
 //
 // Grid: (chunk of 1024 input tokens, request, slice); the slice count is chosen
 // so that the launch has about 2048 workgroups.  Each workgroup
-//   1. counts the kept tokens of its request before its chunk (16-byte role
-//      loads, byte-wise compare, popcount, workgroup sum);
-//   2. ranks the kept tokens of its chunk with wave ballots and an LDS scan
-//      and lists their positions in LDS;
-//   3. copies its slice of those rows (K and V, bitwise) with 16-byte vector
-//      loads and stores; dropped rows are never read.
+//   1. requests the status word, the request's bounds, first cache row and
+//      capacity together;
+//   2. requests every role byte it needs at once: the request's tokens before its
+//      chunk (16-byte loads, counted four bytes at a time) and its own chunk's
+//      (four per thread, in rank order);
+//   3. sums the first and ranks the second in one two-value workgroup scan, and
+//      lists the chunk's kept positions in LDS;
+//   4. copies its slice of those rows (K and V, bitwise), every load of a
+//      thread's batch in flight before its stores; dropped rows are never read.
+// So a workgroup waits for three memory round trips (bounds, roles, rows), and
+// the role bytes a request shares between its chunks are served from L2.
 // Destination row = cache_row_off[b] + (kept before) + rank.  Rows past the
 // request's capacity are not written; SONIC_ERR_CAPACITY is raised instead.
+// role is read only inside its total_tokens bytes.
 #include "common.h"
 #include "scan.h"
 
@@ -19,40 +25,19 @@ namespace sonic {
 constexpr int kCompactThreads = 256;
 constexpr int kCompactChunk = 1024;   // input tokens per workgroup
 constexpr int kCompactMaxSlices = 32; // workgroups sharing one chunk's copy (grid z)
+constexpr int kCountUnroll = 8;       // 16-byte role loads in flight per thread
+constexpr int kCopyUnroll = 4;        // 16-byte K and V units in flight per thread
 
-// Kept (non-history-text) bytes of one 32-bit word, restricted to byte lanes [lo, hi).
-__device__ __forceinline__ int kept_bytes(uint32_t w, int lo, int hi) {
-  int c = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int byte = (w >> (8 * j)) & 0xFF;
-    c += (j >= lo && j < hi && byte != kText) ? 1 : 0;
-  }
-  return c;
-}
-
-// Kept tokens among role[a, e) (absolute byte positions), summed over the workgroup.
-__device__ int count_kept(const uint8_t *__restrict__ role, long a, long e, int *lds) {
-  int c = 0;
-  if (e > a) {
-    const long w0 = a & ~15L;                       // first 16-byte word touching [a, e)
-    const long nwords = ((e + 15) & ~15L) - w0;     // bytes spanned by whole words
-    for (long off = static_cast<long>(threadIdx.x) * 16; off < nwords; off += kCompactThreads * 16) {
-      const long wb = w0 + off;
-      // The aligned 16-byte word holds at least one byte of [a, e), so it lies on a mapped page.
-      const u32x4 x = *reinterpret_cast<const u32x4 *>(role + wb);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const long db = wb + 4 * i;
-        const int lo = static_cast<int>(max(0L, min(4L, a - db)));
-        const int hi = static_cast<int>(max(0L, min(4L, e - db)));
-        c += kept_bytes(x[i], lo, hi);
-      }
-    }
-  }
-  int total;
-  block_int_scan<kCompactThreads>(c, &total, lds);
-  return total;
+// Kept (not HISTORY_TEXT) bytes of a 32-bit word among its byte lanes [lo, hi).
+// Bytes outside the lanes are replaced by the text code; then a byte is dropped
+// exactly when it equals the text code, i.e. when y = w ^ 0x01010101 has a zero
+// byte, counted with the exact zero-byte test ((y & 7f..) + 7f..) | y.
+__device__ __forceinline__ int kept_in_dword(uint32_t w, int lo, int hi) {
+  const uint32_t m = static_cast<uint32_t>(((1ull << (8 * hi)) - 1) & ~((1ull << (8 * lo)) - 1));
+  const uint32_t x = (w & m) | (0x01010101u & ~m);
+  const uint32_t y = x ^ 0x01010101u;
+  const uint32_t zero_hi = ~(((y & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | y) & 0x80808080u;
+  return 4 - __popc(zero_hi);
 }
 
 template <int D>
@@ -61,27 +46,70 @@ __global__ __launch_bounds__(kCompactThreads) void compact_kernel(
     const uint16_t *__restrict__ v, uint16_t *__restrict__ kc, uint16_t *__restrict__ vc,
     const int64_t *__restrict__ row_off, const int32_t *__restrict__ row_cap, int32_t *__restrict__ cache_len,
     int32_t *__restrict__ keep_idx, int32_t *status, int total_tokens, int Hkv) {
-  __shared__ int lds[kCompactThreads / kWave + 1];
+  __shared__ int lds[2 * (kCompactThreads / kWave)];
   __shared__ int16_t kept_pos[kCompactChunk];
   __shared__ int s_ok;
-  if (!block_status_clear(status, &s_ok)) return;
   const int chunk = blockIdx.x;
   const int b = blockIdx.y;
   const int slice = blockIdx.z;
+  // one round trip: status, bounds, first cache row and capacity
   const int s = cu[b];
   const int e = cu[b + 1];
+  const int cap = row_cap[b];
+  const int64_t off0 = row_off[b];
+  if (threadIdx.x == 0) s_ok = __hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0;
+  __syncthreads();
+  if (!s_ok) return;
   if (s < 0 || e < s || e > total_tokens) {   // cu_seqlens itself is malformed
     if (threadIdx.x == 0) raise_status(status, SONIC_ERR_BAD_LAYOUT);
     return;
   }
   const int L = e - s;
-  const int nchunks = (L + kCompactChunk - 1) / kCompactChunk;
-  if (chunk >= max(nchunks, 1)) return;
+  const int nchunks = max((L + kCompactChunk - 1) / kCompactChunk, 1);
+  if (nchunks > static_cast<int>(gridDim.x)) {
+    // max_seqlen understated this request's length: none of its chunks copies anything
+    if (chunk == 0 && slice == 0 && threadIdx.x == 0) raise_status(status, SONIC_ERR_INVALID_ARG);
+    return;
+  }
+  if (chunk >= nchunks) return;
   const int c0 = chunk * kCompactChunk;
 
-  const int before = count_kept(role, s, s + min(c0, L), lds);
-
-  // rank the kept tokens of this chunk: thread t looks at tokens c0 + 4t .. 4t+3
+  // ---- kept tokens before the chunk: role bytes [s, s + c0) in 16-byte words ----
+  int before_part = 0;
+  {
+    const long a = s, z = static_cast<long>(s) + c0;
+    const long w_lo = a & ~15L;
+    const long w_hi = (z + 15) & ~15L;
+    for (long base = w_lo + 16L * threadIdx.x; base < w_hi; base += 16L * kCompactThreads * kCountUnroll) {
+      u32x4 x[kCountUnroll];
+#pragma unroll
+      for (int i = 0; i < kCountUnroll; ++i) {
+        const long wb = base + 16L * kCompactThreads * i;
+        x[i] = u32x4{0x01010101u, 0x01010101u, 0x01010101u, 0x01010101u};
+        if (wb + 16 <= total_tokens) {
+          if (wb < w_hi) x[i] = *reinterpret_cast<const u32x4 *>(role + wb);
+        } else if (wb < w_hi) {   // the array's last, partial word: byte loads inside the array
+#pragma unroll
+          for (int j = 0; j < 16; ++j)
+            if (wb + j < total_tokens)
+              x[i][j / 4] = (x[i][j / 4] & ~(0xFFu << (8 * (j % 4)))) |
+                            (static_cast<uint32_t>(role[wb + j]) << (8 * (j % 4)));
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < kCountUnroll; ++i) {
+        const long wb = base + 16L * kCompactThreads * i;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const long db = wb + 4 * j;
+          const int lo = static_cast<int>(max(0L, min(4L, a - db)));
+          const int hi = static_cast<int>(max(0L, min(4L, z - db)));
+          before_part += kept_in_dword(x[i][j], lo, hi);
+        }
+      }
+    }
+  }
+  // ---- this chunk: thread t looks at tokens c0 + 4t .. 4t+3 ----
   constexpr int PER = kCompactChunk / kCompactThreads;
   bool keep[PER];
   int mine = 0;
@@ -91,17 +119,19 @@ __global__ __launch_bounds__(kCompactThreads) void compact_kernel(
     keep[j] = i < L && role[s + i] != kText;
     mine += keep[j];
   }
-  int chunk_kept;
-  int rank = block_int_scan<kCompactThreads>(mine, &chunk_kept, lds);
+  int x2[2] = {before_part, mine}, below[2], total[2];
+  block_int_scan_n<kCompactThreads, 2>(x2, below, total, lds);
+  const int before = total[0];
+  const int chunk_kept = total[1];
+  int rank = below[1];
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
     if (keep[j]) kept_pos[rank++] = static_cast<int16_t>(PER * threadIdx.x + j);
   }
   __syncthreads();
 
-  const int cap = row_cap[b];
-  const int64_t dst0 = row_off[b] + before;
-  if (chunk == max(nchunks, 1) - 1 && slice == 0 && threadIdx.x == 0) {
+  const int64_t dst0 = off0 + before;
+  if (chunk == nchunks - 1 && slice == 0 && threadIdx.x == 0) {
     const int n = before + chunk_kept;
     if (n > cap) raise_status(status, SONIC_ERR_CAPACITY);
     else cache_len[b] = n;
@@ -118,16 +148,33 @@ __global__ __launch_bounds__(kCompactThreads) void compact_kernel(
   constexpr int UNITS = D / 8;                 // 16-byte units per head row
   const int row_units = Hkv * UNITS;           // 16-byte units per token row
   for (int j = j0 + threadIdx.x; j < jend; j += kCompactThreads) keep_idx[dst0 + j] = c0 + kept_pos[j];
-  const int total = (jend - j0) * row_units;
-  for (int u = threadIdx.x; u < total; u += kCompactThreads) {
-    const int j = j0 + u / row_units;
-    const int w = u % row_units;
-    const size_t src = (static_cast<size_t>(s) + c0 + kept_pos[j]) * row_units + w;
-    const size_t dst = static_cast<size_t>(dst0 + j) * row_units + w;
-    const u32x4 ku = reinterpret_cast<const u32x4 *>(k)[src];
-    const u32x4 vu = reinterpret_cast<const u32x4 *>(v)[src];
-    reinterpret_cast<u32x4 *>(kc)[dst] = ku;
-    reinterpret_cast<u32x4 *>(vc)[dst] = vu;
+  const int nunits = (jend - j0) * row_units;
+  const u32x4 *ks = reinterpret_cast<const u32x4 *>(k);
+  const u32x4 *vs = reinterpret_cast<const u32x4 *>(v);
+  u32x4 *kd = reinterpret_cast<u32x4 *>(kc);
+  u32x4 *vd = reinterpret_cast<u32x4 *>(vc);
+  for (int u0 = threadIdx.x; u0 < nunits; u0 += kCompactThreads * kCopyUnroll) {
+    u32x4 ku[kCopyUnroll], vu[kCopyUnroll];
+    size_t dst[kCopyUnroll];
+#pragma unroll
+    for (int i = 0; i < kCopyUnroll; ++i) {
+      const int u = u0 + i * kCompactThreads;
+      if (u < nunits) {
+        const int j = j0 + u / row_units;
+        const int w = u % row_units;
+        const size_t src = (static_cast<size_t>(s) + c0 + kept_pos[j]) * row_units + w;
+        dst[i] = static_cast<size_t>(dst0 + j) * row_units + w;
+        ku[i] = ks[src];
+        vu[i] = vs[src];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kCopyUnroll; ++i) {
+      if (u0 + i * kCompactThreads < nunits) {
+        kd[dst[i]] = ku[i];
+        vd[dst[i]] = vu[i];
+      }
+    }
   }
 }
 

@@ -110,12 +110,18 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
   const int kvh = blockIdx.y;
   const int b = blockIdx.z;
   const int Hq = Hkv * G;
+  // the status word, the length and the request's first cache row are requested
+  // together (one round trip for all three)
+  const int32_t pending = __hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const int len = cache_len[b];
   const int cap = row_cap[b];
-  // the request's first cache row is requested with its length (one round trip for
-  // both, not a second one after the capacity check)
   const int64_t base = row_off[b];
   asm volatile("" ::"s"(base));
+  // A pending error other than a capacity error (a layout error of an earlier call)
+  // stops the whole call: nothing is appended, written or advanced.  Only capacity
+  // errors can appear during the call (raised below, per request), so every
+  // workgroup of the call takes the same decision and no counter is touched.
+  if (pending != 0 && pending != SONIC_ERR_CAPACITY) return;
   const int n_ctx = len + 1;
   if (n_ctx > cap || n_ctx > max_ctx) {   // uniform over the request: no append, no output
     if (split == 0 && kvh == 0 && threadIdx.x == 0) raise_status(status, SONIC_ERR_CAPACITY);

@@ -177,7 +177,7 @@ def segment_attn_prefill(cu_seqlens, role, turn_id, q, k, v, out, workspace, dev
            key_weight=(key_weight, _F32))
     T, Hq, d = q.shape
     Hkv = k.shape[1]
-    scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    scale = 0.0 if softmax_scale is None else float(softmax_scale)   # 0: the library's 1/sqrt(d)
     return int(lib().sonic_segment_attn_prefill(
         cu_seqlens.numel() - 1, T, Hq, Hkv, d, _ptr(cu_seqlens), _ptr(role), _ptr(turn_id), _ptr(q), _ptr(k),
         _ptr(v), scale, int(nexus_scope), _ptr(out), _ptr(nexus_mass), _ptr(key_weight), _ptr(workspace),
@@ -215,7 +215,7 @@ def compressed_decode(k_cache, v_cache, cache_row_off, cache_row_cap, cache_len,
            v_new=(v_new, _BF16), out=(out, _F32), dev_status=(dev_status, _I32), row_role=(row_role, _U8))
     B, Hq, d = q.shape
     Hkv = k_new.shape[1]
-    scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    scale = 0.0 if softmax_scale is None else float(softmax_scale)   # 0: the library's 1/sqrt(d)
     return int(lib().sonic_compressed_decode(
         B, Hq, Hkv, d, int(max_ctx), _ptr(k_cache), _ptr(v_cache), _ptr(cache_row_off), _ptr(cache_row_cap),
         _ptr(cache_len), _ptr(row_role), _ptr(q), _ptr(k_new), _ptr(v_new), scale, _ptr(out), _ptr(workspace),
@@ -237,7 +237,7 @@ def nexus_extend(nexus_cu, keep_len, k_cache, v_cache, cache_row_off, cache_row_
            q=(q, _BF16), k=(k, _BF16), v=(v, _BF16), out=(out, _F32), dev_status=(dev_status, _I32))
     N, Hq, d = q.shape
     Hkv = k.shape[1]
-    scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    scale = 0.0 if softmax_scale is None else float(softmax_scale)   # 0: the library's 1/sqrt(d)
     return int(lib().sonic_nexus_extend(
         nexus_cu.numel() - 1, N, Hq, Hkv, d, int(max_rows), _ptr(nexus_cu), _ptr(keep_len), _ptr(k_cache),
         _ptr(v_cache), _ptr(cache_row_off), _ptr(cache_row_cap), _ptr(cache_len), _ptr(q), _ptr(k), _ptr(v), scale,

@@ -39,23 +39,46 @@ def assert_close(got, want, what):
     return mx, mean
 
 
+def run_starts(lay: W.RequestLayout):
+    """Request-local starts of the runs (maximal ranges of one role and one segment)."""
+    role, turn = lay.roles_and_turns()
+    return [0] + [i for i in range(1, lay.length) if role[i] != role[i - 1] or turn[i] != turn[i - 1]]
+
+
 def sample_rows(lay: W.RequestLayout, rng, every=None, extra=16):
     """Request-local rows to check: the first and last row of every run, rows around every
-    32-row block edge inside runs, and a few random rows."""
-    role, turn = lay.roles_and_turns()
+    32-row block edge inside runs, the last row of every 32-row block of the request, and a
+    few random rows."""
     L = lay.length
     if L == 0:
         return np.zeros(0, np.int64)
     rows = set([0, L - 1])
-    starts = [0] + [i for i in range(1, L) if role[i] != role[i - 1] or turn[i] != turn[i - 1]]
-    for s in starts:
+    for s in run_starts(lay):
         for r in (s - 1, s, s + 1, s + 31, s + 32, s + 33):
             if 0 <= r < L:
                 rows.add(r)
+    rows.update(range(31, L, 32))
     rows.update(int(x) for x in rng.integers(0, L, size=extra))
     if every:
         rows.update(range(0, L, every))
     return np.array(sorted(rows), np.int64)
+
+
+def subset_rows(lay: W.RequestLayout, margin=64, every=16):
+    """The deterministic row subset of a long request: every system, Nexus and current row;
+    the `margin` rows on either side of every run boundary; every `every`-th body row; and the
+    last row of every 32-row block."""
+    role, _ = lay.roles_and_turns()
+    L = lay.length
+    keep = role != W.ROLE_HISTORY_TEXT
+    for s in run_starts(lay):
+        keep[max(0, s - margin):min(L, s + margin)] = True
+    body = np.flatnonzero(role == W.ROLE_HISTORY_TEXT)
+    keep[body[body % every == 0]] = True
+    keep[31::32] = True
+    if L:
+        keep[L - 1] = True
+    return np.flatnonzero(keep).astype(np.int64)
 
 
 def oracle_prefill_rows(batch: W.Batch, rows_per_req, nexus_scope=OM.NEXUS_ALL):

@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert sonic.abi_version() == 7
+    assert sonic.abi_version() == 8
     assert sonic.status_string(0) == "ok"
     for code in range(1, 7):
         assert sonic.status_string(code) != "unknown status"
@@ -132,3 +132,30 @@ def test_workspace_sizes():
     assert sonic.prefill_workspace_bytes(1, 10, 4, 0, 64) == 0
     assert sonic.prefill_workspace_bytes(1, 10, 0, 2, 64) == 0
     assert sonic.decode_workspace_bytes(8, 32, 128, 1584) >= 8 * 32 * 130 * 4
+
+
+def test_softmax_scale_argument_checks_without_gpu():
+    """softmax_scale = 0 selects 1/sqrt(d) inside the C ABI; a negative or non-finite scale is an
+    argument error.  An empty batch returns before any GPU call, so this runs on the CPU."""
+    L = sonic.lib()
+    st = ctypes.c_int32(0)
+    sp = ctypes.byref(st)
+    n = None
+
+    def prefill(scale):
+        return L.sonic_segment_attn_prefill(0, 0, 4, 2, 64, n, n, n, n, n, n, scale, 0, n, n, n, n, 0, sp, n)
+
+    def decode(scale):
+        return L.sonic_compressed_decode(0, 4, 2, 64, 16, n, n, n, n, n, n, n, n, n, scale, n, n, 0, sp, n)
+
+    def extend(scale):
+        return L.sonic_nexus_extend(0, 0, 4, 2, 64, 16, n, n, n, n, n, n, n, n, n, n, scale, n, n, 0, sp, n)
+
+    for call in (prefill, decode, extend):
+        assert call(0.0) == sonic.OK
+        assert call(-0.0) == sonic.OK
+        assert call(0.125) == sonic.OK
+        assert call(-0.125) == sonic.ERR_INVALID_ARG
+        assert call(float("nan")) == sonic.ERR_INVALID_ARG
+        assert call(float("inf")) == sonic.ERR_INVALID_ARG
+    assert st.value == 0

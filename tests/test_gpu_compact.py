@@ -83,3 +83,23 @@ def test_compact_capacity_overflow_stays_inside_capacity():
     for j in range(int(caps[1])):
         row = k[start1 + j]
         assert np.all(row == 0xFFFF) or np.array_equal(row, kc[int(kept[0]) + j]), j
+
+
+def test_compact_understated_max_seqlen_is_an_error_and_writes_nothing():
+    """The grid is sized from max_seqlen; a longer request raises INVALID_ARG and none of its rows is
+    written."""
+    lays = [W.RequestLayout(300, [900], [200], 1200), W.RequestLayout(10, [50], [5], 5)]
+    batch = W.make_batch("maxlen", lays, 2, 2, 64, seed=6)
+    caps = H.kept_counts(batch)
+    H.need_gpu()
+    db = H.device_batch(batch)
+    cache = db.alloc_cache(caps)
+    st = sonic.kv_compact(db.cu, db.role, db.k, db.v, cache.k, cache.v, cache.row_off, cache.row_cap, cache.length,
+                          cache.keep_idx, db.status, max_seqlen=1024)
+    assert st == sonic.OK
+    torch.cuda.synchronize()
+    assert db.read_status() == sonic.ERR_INVALID_ARG
+    k = bf16_to_host(cache.k)
+    assert np.all(k[:int(caps[0])] == 0xFFFF)
+    assert np.all(cache.keep_idx.cpu().numpy()[:int(caps[0])] == -1)
+    assert cache.length.cpu().numpy()[0] == 0

@@ -169,3 +169,60 @@ def test_decode_capacity_overflow():
     want = OD.decode_step(batch.dec_q[1, 1], np.concatenate([kc[o:o + ln], batch.dec_k[:1, 1]]),
                           np.concatenate([vc[o:o + ln], batch.dec_v[:1, 1]]), batch.dec_k[1, 1], batch.dec_v[1, 1])
     H.assert_close(got[1], want, "request 1 after request 0 overflowed")
+
+
+def test_decode_honours_pending_layout_error():
+    """A layout error left by an earlier call stops decode (no append, no output, no length change);
+    a pending capacity error does not (capacity is per request); afterwards decode still matches the
+    oracle, so the split counters were left consistent."""
+    H.need_gpu()
+    # long enough contexts for several splits per (request, kv-head) pair
+    lays = [W.RequestLayout(700, [30], [12], 9), W.RequestLayout(650, [20], [4], 3)]
+    steps = 2
+    batch = W.make_batch("pending", lays, 8, 2, 128, seed=4, decode_steps=steps)
+    db, cache, ref = compacted(batch, steps)
+    kc, vc, n, off = ref
+    max_ctx = int(cache.row_cap_host.max())
+    out = torch.full((2, 8, 128), 5.0, dtype=torch.float32, device="cuda")
+    q, kn, vn = (bf16_to_device(x) for x in (batch.dec_q, batch.dec_k, batch.dec_v))
+    k_before, v_before = bf16_to_host(cache.k).copy(), bf16_to_host(cache.v).copy()
+    db.status.fill_(sonic.ERR_BAD_LAYOUT)
+    assert cache.decode(q[0], kn[0], vn[0], out, db.status, max_ctx) == sonic.OK
+    torch.cuda.synchronize()
+    assert db.read_status() == sonic.ERR_BAD_LAYOUT
+    assert np.array_equal(cache.length.cpu().numpy(), n)
+    assert torch.all(out == 5.0)
+    assert np.array_equal(bf16_to_host(cache.k), k_before) and np.array_equal(bf16_to_host(cache.v), v_before)
+    ctx = compact_ctx_fn(batch, ref)
+    db.status.fill_(sonic.ERR_CAPACITY)
+    for t in range(steps):
+        assert cache.decode(q[t], kn[t], vn[t], out, db.status, max_ctx) == sonic.OK
+        torch.cuda.synchronize()
+        assert db.read_status() == (sonic.ERR_CAPACITY if t == 0 else 0)
+        got = out.cpu().numpy()
+        for b in range(2):
+            kk, vv = ctx(b, t)
+            want = OD.decode_step(batch.dec_q[t, b], kk, vv, batch.dec_k[t, b], batch.dec_v[t, b])
+            H.assert_close(got[b], want, f"step {t} request {b} after a pending status")
+        db.clear_status()
+    assert np.array_equal(cache.length.cpu().numpy(), n + steps)
+
+
+def test_decode_default_scale_is_one_over_sqrt_d():
+    """softmax_scale = 0 (the binding's default) gives bit for bit the output of an explicit 1/sqrt(d)."""
+    H.need_gpu()
+    lays = [W.RequestLayout(40, [30], [12], 9), W.RequestLayout(3, [20], [4], 3)]
+    batch = W.make_batch("scale", lays, 8, 2, 64, seed=5, decode_steps=1)
+    outs = []
+    for scale in (None, 1.0 / np.sqrt(64.0)):
+        db, cache, ref = compacted(batch, 1)
+        out = torch.empty((2, 8, 64), dtype=torch.float32, device="cuda")
+        st = sonic.compressed_decode(cache.k, cache.v, cache.row_off, cache.row_cap, cache.length,
+                                     bf16_to_device(batch.dec_q[0]), bf16_to_device(batch.dec_k[0]),
+                                     bf16_to_device(batch.dec_v[0]), out,
+                                     torch.zeros(sonic.decode_workspace_bytes(2, 8, 64, 64), dtype=torch.uint8,
+                                                 device="cuda"), db.status, 64, softmax_scale=scale)
+        assert st == sonic.OK
+        torch.cuda.synchronize()
+        outs.append(out.cpu().numpy())
+    assert np.array_equal(outs[0], outs[1])
