@@ -106,6 +106,23 @@ __device__ __forceinline__ float pair16_add(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Sum of the bf16 values of a packed operand, in fp32: v_dot2c_f32_bf16 against (1, 1)
+// adds one pair per instruction, four independent chains.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+template <int N>
+__device__ __forceinline__ float rounded_sum(const bf16x8 (&p)[N]) {
+  const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    acc[0] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p[i], p[i], 0, 1), ones, acc[0], false);
+    acc[1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p[i], p[i], 2, 3), ones, acc[1], false);
+    acc[2] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p[i], p[i], 4, 5), ones, acc[2], false);
+    acc[3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p[i], p[i], 6, 7), ones, acc[3], false);
+  }
+  return (acc[0] + acc[1]) + (acc[2] + acc[3]);
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 

@@ -11,7 +11,8 @@
 //            a column's statistics live in the four lanes that hold it;
 //   values   O^T (d x 16 cols) += V^T . P^T   v_mfma_f32_16x16x16_bf16, V read
 //            back transposed (ds_read_b64_tr_b16); P^T is the score accumulator
-//            itself, rounded to bf16 (its lane layout is the operand layout).
+//            itself, rounded to bf16 (its lane layout is the operand layout), and
+//            the softmax sum adds those rounded values.
 // K and V rows go straight from global memory to a two-slot LDS ring of the
 // wave's own (direct-to-LDS loads), so a wave keeps its next group in flight
 // while it computes one.  The waves then merge through LDS.
@@ -317,11 +318,16 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
     }
     f32x4 p;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      p[i] = (x[i] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(x[i] - m_run);
-      l_run += p[i];
+    for (int i = 0; i < 4; ++i) p[i] = (x[i] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(x[i] - m_run);
+    const bf16x4 pr = __builtin_convertvector(p, bf16x4);
+    const v4i16 pb = __builtin_bit_cast(v4i16, pr);
+    // the sum is taken over the rounded probabilities the value product uses, so the
+    // output stays a convex combination of the V rows (see the prefill)
+    {
+      const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pr, pr, 0, 1), ones, l_run, false);
+      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pr, pr, 2, 3), ones, l_run, false);
     }
-    const v4i16 pb = __builtin_bit_cast(v4i16, __builtin_convertvector(p, bf16x4));
     const uint16_t *vslot = kslot + SLOT;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {

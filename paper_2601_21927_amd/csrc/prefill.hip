@@ -7,7 +7,8 @@
 //
 //   S^T (64 keys x 32 rows)   = K . Q^T   v_mfma_f32_32x32x16_bf16, fp32 accumulate
 //   online softmax over keys  (fp32, exp2 with log2(e) folded into the scale)
-//   O^T (d x 32 rows)        += V^T . P^T  v_mfma_f32_32x32x16_bf16, P rounded to bf16
+//   O^T (d x 32 rows)        += V^T . P^T  v_mfma_f32_32x32x16_bf16, P rounded to bf16;
+//                              the softmax sum adds the rounded values
 //
 // Computing the transposed products leaves each lane with one query row
 // (lane % 32) in every accumulator, so row maxima and sums need a single
@@ -269,8 +270,9 @@ __global__ __launch_bounds__(G * kWave * KS, 3 - KS) void prefill_kernel(AttnRow
 #pragma unroll
     for (int i = 0; i < DB; ++i) oacc[i] = f32x16{};
     float m_run = -INFINITY;   // running max in the log2 domain (lags by at most kLazy)
-    float l_run = 0.f;
-    float l_nex = 0.f;         // STATS: the part of l_run from Nexus keys
+    float l_run = 0.f;         // sum of the bf16-rounded probabilities the P.V product uses
+    float l_ex = 0.f;          // STATS: the same sum before rounding (normaliser, Nexus mass)
+    float l_nex = 0.f;         // STATS: the part of l_ex from Nexus keys
     // STATS: Nexus keys are the virtual keys [nex_lo, npre) (the prefix past the system rows)
     const int nex_lo = STATS ? min(ws.req[t.req].system, npre) : npre;
 
@@ -333,7 +335,10 @@ __global__ __launch_bounds__(G * kWave * KS, 3 - KS) void prefill_kernel(AttnRow
         const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
         m_run = m_new;
         l_run *= corr;
-        if (STATS) l_nex *= corr;
+        if (STATS) {
+          l_ex *= corr;
+          l_nex *= corr;
+        }
 #pragma unroll
         for (int db = 0; db < DB; ++db) oacc[db] *= corr;
       }
@@ -350,7 +355,7 @@ __global__ __launch_bounds__(G * kWave * KS, 3 - KS) void prefill_kernel(AttnRow
         for (int e = 0; e < 8; ++e) {
           lo[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][e], scale_log2, -m_run));
           hi[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][8 + e], scale_log2, -m_run));
-          lsum += lo[e] + hi[e];
+          if (STATS) lsum += lo[e] + hi[e];
           if (nex_some) {
             const int klo = kb * 32 + acc_key(e, g), khi = kb * 32 + acc_key(8 + e, g);
             nsum += ((klo >= nx0 && klo < nx1) ? lo[e] : 0.f) + ((khi >= nx0 && khi < nx1) ? hi[e] : 0.f);
@@ -359,7 +364,13 @@ __global__ __launch_bounds__(G * kWave * KS, 3 - KS) void prefill_kernel(AttnRow
         pb[2 * kb] = __builtin_convertvector(lo, bf16x8);
         pb[2 * kb + 1] = __builtin_convertvector(hi, bf16x8);
       }
-      l_run += lsum;
+      // The output is normalised by the sum of the rounded probabilities themselves, so
+      // that it stays a convex combination of the V rows: a row dominated by one key then
+      // loses nothing to the rounding of that key's probability (which the lagging max
+      // leaves anywhere in [1, 2^8), not exactly 1).  v_dot2c_f32_bf16 against (1, 1)
+      // adds a packed pair of them in one instruction.
+      l_run += rounded_sum(pb);
+      if (STATS) l_ex += lsum;
       if (nex_all) l_nex += lsum;
       if (nex_some) l_nex += nsum;
 
@@ -437,10 +448,11 @@ __global__ __launch_bounds__(G * kWave * KS, 3 - KS) void prefill_kernel(AttnRow
     const float inv = 1.f / l_tot;
     if (STATS) {
       const float n_tot = pair32_add(l_nex);
+      const float x_tot = pair32_add(l_ex);
       if (n < t.nrows && g == 0) {
         const size_t idx = static_cast<size_t>(base + t.p0 + n) * Hq + h;
-        if (rows.nexus_mass != nullptr) rows.nexus_mass[idx] = n_tot * inv;
-        rows.lse[idx] = m_run + __builtin_amdgcn_logf(l_tot);
+        if (rows.nexus_mass != nullptr) rows.nexus_mass[idx] = n_tot / x_tot;
+        rows.lse[idx] = m_run + __builtin_amdgcn_logf(x_tot);
       }
     }
     if (n < t.nrows) {
