@@ -339,6 +339,29 @@ int32_t sonic_compressed_decode(int32_t batch, int32_t num_q_heads, int32_t num_
                                 float *out, void *workspace, size_t workspace_bytes, int32_t *dev_status,
                                 void *stream);
 
+/*
+ * The same decode step as sonic_compressed_decode, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation): no workspace argument, and the call allocates nothing.  Its
+ * completion counters and split partials live in one fixed device array of 8 MiB per
+ * GPU that the library holds until the process ends; the counters sit in its first
+ * 64 KiB, at the same place for every call, and every call leaves them at zero (the
+ * first call on a GPU also enqueues a small kernel on `stream` that clears them).
+ * Arguments, outputs and errors are those of sonic_compressed_decode, plus:
+ *   - SONIC_ERR_WORKSPACE (returned, nothing enqueued) when the call needs more than
+ *     the array holds: batch > 4096, batch * num_kv_heads > 12288, or more than
+ *     8 MiB - 64 KiB of partials (batch * num_q_heads * splits * (head_dim + 2) * 4 B,
+ *     splits as sonic_decode_workspace_bytes counts them);
+ *   - calls on one GPU share the array, so calls that overlap on it (concurrent
+ *     streams, other threads) race; calls ordered on one stream do not.
+ */
+int32_t sonic_compressed_decode_noalloc(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                        int32_t head_dim, int32_t max_ctx, void *k_cache, void *v_cache,
+                                        const int64_t *cache_row_off, const int32_t *cache_row_cap,
+                                        int32_t *cache_len, const uint8_t *row_role, const void *q,
+                                        const void *k_new, const void *v_new, float softmax_scale, float *out,
+                                        int32_t *dev_status, void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* Next turn: the ended turn's Nexus tokens over the compact cache            */
 /* ------------------------------------------------------------------------ */

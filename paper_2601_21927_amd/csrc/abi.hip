@@ -38,14 +38,17 @@ hipError_t launch_compact(int batch, int total_tokens, int max_seqlen, int Hkv, 
                           const int32_t *row_cap, int32_t *cache_len, int32_t *keep_idx, int32_t *status,
                           hipStream_t stream);
 int decode_splits(int batch, int Hkv, int max_ctx);
+size_t decode_ws_layout(int batch, int Hkv, int G, int D, int nsplit, DecodeWs *ws, char *base);
+size_t decode_scratch_layout(int batch, int Hkv, int G, int D, int nsplit, DecodeWs *ws, char *base);
+hipError_t decode_scratch(hipStream_t stream, char **base);
 hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int nsplit, uint16_t *kc,
                          uint16_t *vc, const int64_t *row_off, const int32_t *row_cap, int32_t *cache_len,
                          const uint8_t *row_role, const uint16_t *q, const uint16_t *k_new, const uint16_t *v_new,
-                         float scale_log2, float *out, void *ws, int32_t *status, hipStream_t stream);
+                         float scale_log2, float *out, const DecodeWs &ws, int32_t *status, hipStream_t stream);
 
 namespace {
 
-constexpr int kAbiVersion = 8;
+constexpr int kAbiVersion = 9;
 constexpr double kLog2e = 1.4426950408889634;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -539,33 +542,78 @@ size_t sonic_decode_workspace_bytes(int32_t batch, int32_t Hq, int32_t d, int32_
   return align_up(decode_ws_bytes(batch, Hq, d, decode_splits(batch, 1, max_ctx)), 256);
 }
 
+// Argument checks shared by the two decode entry points.  Returns SONIC_OK with *empty set
+// when there is nothing to do, or the status to return.
+static int32_t check_decode(int32_t batch, int32_t Hq, int32_t Hkv, int32_t d, int32_t max_ctx, const void *k_cache,
+                            const void *v_cache, const int64_t *cache_row_off, const int32_t *cache_row_cap,
+                            const int32_t *cache_len, const void *q, const void *k_new, const void *v_new,
+                            float *softmax_scale, const float *out, const int32_t *dev_status, bool *empty) {
+  *empty = false;
+  if (batch < 0 || Hq <= 0 || Hkv <= 0 || max_ctx <= 0 || dev_status == nullptr) return SONIC_ERR_INVALID_ARG;
+  if (d != 64 && d != 128) return SONIC_ERR_UNSUPPORTED;
+  if (Hq % Hkv != 0) return SONIC_ERR_INVALID_ARG;
+  if (Hq / Hkv > 8) return SONIC_ERR_UNSUPPORTED;
+  if (batch > 65535 || Hkv > 65535) return SONIC_ERR_UNSUPPORTED;
+  if (!std::isfinite(*softmax_scale) || *softmax_scale < 0.f) return SONIC_ERR_INVALID_ARG;
+  *softmax_scale = default_scale(*softmax_scale, d);
+  if (batch == 0) {
+    *empty = true;
+    return SONIC_OK;
+  }
+  if (!k_cache || !v_cache || !cache_row_off || !cache_row_cap || !cache_len || !q || !k_new || !v_new || !out)
+    return SONIC_ERR_INVALID_ARG;
+  if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(q, 16) || !aligned(k_new, 16) ||
+      !aligned(v_new, 16) || !aligned(out, 16))
+    return SONIC_ERR_INVALID_ARG;
+  return SONIC_OK;
+}
+
 int32_t sonic_compressed_decode(int32_t batch, int32_t Hq, int32_t Hkv, int32_t d, int32_t max_ctx, void *k_cache,
                                 void *v_cache, const int64_t *cache_row_off, const int32_t *cache_row_cap,
                                 int32_t *cache_len, const uint8_t *row_role, const void *q, const void *k_new,
                                 const void *v_new, float softmax_scale, float *out, void *workspace,
                                 size_t workspace_bytes, int32_t *dev_status, void *stream_) {
   hipStream_t stream = static_cast<hipStream_t>(stream_);
-  if (batch < 0 || Hq <= 0 || Hkv <= 0 || max_ctx <= 0 || dev_status == nullptr) return SONIC_ERR_INVALID_ARG;
-  if (d != 64 && d != 128) return SONIC_ERR_UNSUPPORTED;
-  if (Hq % Hkv != 0) return SONIC_ERR_INVALID_ARG;
-  if (Hq / Hkv > 8) return SONIC_ERR_UNSUPPORTED;
-  if (batch > 65535 || Hkv > 65535) return SONIC_ERR_UNSUPPORTED;
-  if (!std::isfinite(softmax_scale) || softmax_scale < 0.f) return SONIC_ERR_INVALID_ARG;
-  softmax_scale = default_scale(softmax_scale, d);
-  if (batch == 0) return SONIC_OK;
-  if (!k_cache || !v_cache || !cache_row_off || !cache_row_cap || !cache_len || !q || !k_new || !v_new || !out ||
-      !workspace)
-    return SONIC_ERR_INVALID_ARG;
-  if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(q, 16) || !aligned(k_new, 16) ||
-      !aligned(v_new, 16) || !aligned(out, 16) || !aligned(workspace, 256))
-    return SONIC_ERR_INVALID_ARG;
+  bool empty = false;
+  const int32_t st = check_decode(batch, Hq, Hkv, d, max_ctx, k_cache, v_cache, cache_row_off, cache_row_cap,
+                                  cache_len, q, k_new, v_new, &softmax_scale, out, dev_status, &empty);
+  if (st != SONIC_OK || empty) return st;
+  if (!workspace || !aligned(workspace, 256)) return SONIC_ERR_INVALID_ARG;
   const int nsplit = decode_splits(batch, Hkv, max_ctx);
   if (workspace_bytes < decode_ws_bytes(batch, Hq, d, nsplit)) return SONIC_ERR_WORKSPACE;
+  DecodeWs ws;
+  decode_ws_layout(batch, Hkv, Hq / Hkv, d, nsplit, &ws, static_cast<char *>(workspace));
   hipError_t e = launch_decode(batch, Hq, Hkv, d, max_ctx, nsplit, static_cast<uint16_t *>(k_cache),
                                static_cast<uint16_t *>(v_cache), cache_row_off, cache_row_cap, cache_len, row_role,
                                static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k_new),
                                static_cast<const uint16_t *>(v_new), static_cast<float>(softmax_scale * kLog2e), out,
-                               workspace, dev_status, stream);
+                               ws, dev_status, stream);
+  return finish(e, dev_status, stream);
+}
+
+int32_t sonic_compressed_decode_noalloc(int32_t batch, int32_t Hq, int32_t Hkv, int32_t d, int32_t max_ctx,
+                                        void *k_cache, void *v_cache, const int64_t *cache_row_off,
+                                        const int32_t *cache_row_cap, int32_t *cache_len, const uint8_t *row_role,
+                                        const void *q, const void *k_new, const void *v_new, float softmax_scale,
+                                        float *out, int32_t *dev_status, void *stream_) {
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  bool empty = false;
+  const int32_t st = check_decode(batch, Hq, Hkv, d, max_ctx, k_cache, v_cache, cache_row_off, cache_row_cap,
+                                  cache_len, q, k_new, v_new, &softmax_scale, out, dev_status, &empty);
+  if (st != SONIC_OK || empty) return st;
+  const int nsplit = decode_splits(batch, Hkv, max_ctx);
+  const size_t need = decode_scratch_layout(batch, Hkv, Hq / Hkv, d, nsplit, nullptr, nullptr);
+  if (need == 0 || need > kScratchBytes) return SONIC_ERR_WORKSPACE;
+  char *base = nullptr;
+  hipError_t e = decode_scratch(stream, &base);
+  if (e != hipSuccess) return SONIC_ERR_HIP;
+  DecodeWs ws;
+  decode_scratch_layout(batch, Hkv, Hq / Hkv, d, nsplit, &ws, base);
+  e = launch_decode(batch, Hq, Hkv, d, max_ctx, nsplit, static_cast<uint16_t *>(k_cache),
+                    static_cast<uint16_t *>(v_cache), cache_row_off, cache_row_cap, cache_len, row_role,
+                    static_cast<const uint16_t *>(q), static_cast<const uint16_t *>(k_new),
+                    static_cast<const uint16_t *>(v_new), static_cast<float>(softmax_scale * kLog2e), out, ws,
+                    dev_status, stream);
   return finish(e, dev_status, stream);
 }
 

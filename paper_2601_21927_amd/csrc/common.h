@@ -205,4 +205,19 @@ struct PrefillWs {
   int32_t *ncur;       // [B] current-query rows of request b
 };
 
+// Device workspace of the decode; the counters are zero between calls.
+struct DecodeWs {
+  int32_t *done;      // [B]      kv-heads of request b whose splits have all counted in this call
+  int32_t *arrive;    // [B*Hkv]  splits of a (request, kv-head) finished in this call
+  float *part;        // [B*Hkv][nsplit][G*(D+2)] partial (m[G], l[G], acc[G][D]) per split
+};
+
+// The decode's fixed-layout scratch (the entry point that allocates nothing): counters
+// for up to kScratchMaxRequests requests and kScratchMaxPairs (request, kv-head) pairs,
+// then the partial records, kScratchBytes in all.
+constexpr int kScratchMaxRequests = 4096;
+constexpr int kScratchMaxPairs = 12288;
+constexpr size_t kScratchCounterBytes = (kScratchMaxRequests + kScratchMaxPairs) * sizeof(int32_t);   // 64 KiB
+constexpr size_t kScratchBytes = size_t(8) << 20;
+
 }  // namespace sonic

@@ -36,13 +36,6 @@ constexpr int kDecWaves = 8;
 constexpr int kDecThreads = kDecWaves * kWave;
 constexpr int kGroupRows = 16;
 
-// Device workspace of the decode; the counters are zero between calls.
-struct DecodeWs {
-  int32_t *done;      // [B]      kv-heads of request b whose splits have all counted in this call
-  int32_t *arrive;    // [B*Hkv]  splits of a (request, kv-head) finished in this call
-  float *part;        // [B*Hkv][nsplit][G*(D+2)] partial (m[G], l[G], acc[G][D]) per split
-};
-
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
@@ -424,6 +417,21 @@ int decode_splits(int batch, int Hkv, int max_ctx) {
   return static_cast<int>(s < 1 ? 1 : s);
 }
 
+// Fixed layout of a scratch array shared by calls of different shapes: the counters
+// sit at the same offsets for every call (each call leaves them at zero), the partial
+// records after them.  Returns the bytes a call needs, or 0 when its requests or
+// (request, kv-head) pairs exceed the fixed counter regions.
+size_t decode_scratch_layout(int batch, int Hkv, int G, int D, int nsplit, DecodeWs *ws, char *base) {
+  if (batch > kScratchMaxRequests || static_cast<long>(batch) * Hkv > kScratchMaxPairs) return 0;
+  const size_t pbytes = nsplit > 1 ? static_cast<size_t>(batch) * Hkv * nsplit * G * (D + 2) * sizeof(float) : 0;
+  if (ws) {
+    ws->done = reinterpret_cast<int32_t *>(base);
+    ws->arrive = reinterpret_cast<int32_t *>(base + kScratchMaxRequests * sizeof(int32_t));
+    ws->part = reinterpret_cast<float *>(base + kScratchCounterBytes);
+  }
+  return kScratchCounterBytes + pbytes;
+}
+
 size_t decode_ws_layout(int batch, int Hkv, int G, int D, int nsplit, DecodeWs *ws, char *base) {
   const size_t dbytes = (static_cast<size_t>(batch) * sizeof(int32_t) + 255) / 256 * 256;
   const size_t abytes = (static_cast<size_t>(batch) * Hkv * sizeof(int32_t) + 255) / 256 * 256;
@@ -454,10 +462,8 @@ static void launch_decode_dg(dim3 grid, int batch, int Hkv, int max_ctx, int nsp
 hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int nsplit, uint16_t *kc, uint16_t *vc,
                          const int64_t *row_off, const int32_t *row_cap, int32_t *cache_len, const uint8_t *row_role,
                          const uint16_t *q, const uint16_t *k_new, const uint16_t *v_new, float scale_log2,
-                         float *out, void *ws_base, int32_t *status, hipStream_t stream) {
+                         float *out, const DecodeWs &ws, int32_t *status, hipStream_t stream) {
   const int G = Hq / Hkv;
-  DecodeWs ws;
-  decode_ws_layout(batch, Hkv, G, D, nsplit, &ws, static_cast<char *>(ws_base));
   dim3 grid(nsplit, Hkv, batch);
 #define DEC(DD, GG)                                                                                               \
   case GG:                                                                                                        \

@@ -31,7 +31,8 @@ NEXUS_ALL, NEXUS_UP_TO_OWN = 0, 1   # Nexus <-> Nexus visibility scope of the pr
 EXPORTS = (
     "sonic_abi_version", "sonic_status_string", "sonic_validate_layout_host", "sonic_layout_stats_host",
     "sonic_prefill_workspace_bytes", "sonic_segment_attn_prefill", "sonic_kv_compact",
-    "sonic_decode_workspace_bytes", "sonic_compressed_decode", "sonic_nexus_extend_workspace_bytes",
+    "sonic_decode_workspace_bytes", "sonic_compressed_decode", "sonic_compressed_decode_noalloc",
+    "sonic_nexus_extend_workspace_bytes",
     "sonic_nexus_extend", "sonic_role_projection_workspace_bytes", "sonic_role_projection",
     "sonic_nexus_recon_workspace_bytes", "sonic_nexus_recon_targets",
 )
@@ -75,6 +76,9 @@ def lib() -> ctypes.CDLL:
     L.sonic_compressed_decode.restype = _i32
     L.sonic_compressed_decode.argtypes = [_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _f32,
                                           _p, _p, _sz, _p, _p]
+    L.sonic_compressed_decode_noalloc.restype = _i32
+    L.sonic_compressed_decode_noalloc.argtypes = [_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p,
+                                                  _f32, _p, _p, _p]
     L.sonic_nexus_extend_workspace_bytes.restype = _sz
     L.sonic_nexus_extend_workspace_bytes.argtypes = [_i32, _i32]
     L.sonic_nexus_extend.restype = _i32
@@ -220,6 +224,22 @@ def compressed_decode(k_cache, v_cache, cache_row_off, cache_row_cap, cache_len,
         B, Hq, Hkv, d, int(max_ctx), _ptr(k_cache), _ptr(v_cache), _ptr(cache_row_off), _ptr(cache_row_cap),
         _ptr(cache_len), _ptr(row_role), _ptr(q), _ptr(k_new), _ptr(v_new), scale, _ptr(out), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _ptr(dev_status), _stream(stream)))
+
+
+def compressed_decode_noalloc(k_cache, v_cache, cache_row_off, cache_row_cap, cache_len, q, k_new, v_new, out,
+                              dev_status, max_ctx: int, row_role=None, softmax_scale=None, stream=None) -> int:
+    """compressed_decode without a workspace: the library's fixed per-GPU scratch is used."""
+    _dev(k_cache, v_cache, cache_row_off, cache_row_cap, cache_len, q, k_new, v_new, out, dev_status, row_role)
+    _types(k_cache=(k_cache, _BF16), v_cache=(v_cache, _BF16), cache_row_off=(cache_row_off, _I64),
+           cache_row_cap=(cache_row_cap, _I32), cache_len=(cache_len, _I32), q=(q, _BF16), k_new=(k_new, _BF16),
+           v_new=(v_new, _BF16), out=(out, _F32), dev_status=(dev_status, _I32), row_role=(row_role, _U8))
+    B, Hq, d = q.shape
+    Hkv = k_new.shape[1]
+    scale = 0.0 if softmax_scale is None else float(softmax_scale)   # 0: the library's 1/sqrt(d)
+    return int(lib().sonic_compressed_decode_noalloc(
+        B, Hq, Hkv, d, int(max_ctx), _ptr(k_cache), _ptr(v_cache), _ptr(cache_row_off), _ptr(cache_row_cap),
+        _ptr(cache_len), _ptr(row_role), _ptr(q), _ptr(k_new), _ptr(v_new), scale, _ptr(out), _ptr(dev_status),
+        _stream(stream)))
 
 
 # ----------------------------------------------------------------- next turn: Nexus step

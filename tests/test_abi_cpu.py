@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert sonic.abi_version() == 8
+    assert sonic.abi_version() == 9
     assert sonic.status_string(0) == "ok"
     for code in range(1, 7):
         assert sonic.status_string(code) != "unknown status"
