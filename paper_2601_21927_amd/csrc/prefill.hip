@@ -470,6 +470,233 @@ __global__ __launch_bounds__(G * kWave * KS, 3 - KS) void prefill_kernel(AttnRow
   }
 }
 
+// Ping-pong variant for G > 4 (one key group, one head per wave, no statistics).
+// The waves form two groups, waves [0, 4) and [4, G), one wave of each on a SIMD
+// (a workgroup's waves go to the SIMDs in turn), and the groups run half a step
+// apart, so that in every phase one group runs matrix work while the other runs
+// its softmax and each SIMD overlaps one wave's MFMAs with the other's VALU work:
+//   phase 2c:     group 0: P.V(c-1), S(c)     group 1: softmax(c-1)
+//   phase 2c+1:   group 0: softmax(c)         group 1: P.V(c-1), S(c)
+// (In the single-group kernel the two waves of a SIMD belong to one workgroup and
+// are held in step by its barriers, so their MFMA and VALU phases coincide.)
+// LDS slot c % 2 holds K(c) and V(c-1) through phases 2c and 2c+1.  The first group
+// issues the loads of K(c+1) and V(c) into the other slot at the start of phase 2c,
+// behind the barrier that ends the last use of that slot, and waits for them at the
+// start of phase 2c+2.  Every phase begins with a barrier: two per 64-key step, as
+// in the single-group kernel.  The arithmetic of a row and head is the same as
+// there, in the same order, so the outputs are identical.
+template <int D, int G>
+__global__ __launch_bounds__(G * kWave, 2) void prefill_pp_kernel(AttnRows rows, PrefillWs ws, int Hkv,
+                                                                  float scale_log2) {
+  static_assert(G > 4 && G <= 8, "two groups of waves, the second of G - 4");
+  const uint16_t *__restrict__ q = rows.q;
+  float *__restrict__ out = rows.out;
+  constexpr int DC = D / 8;              // 16-byte chunks per K/V row
+  constexpr int DS = D / 16;             // d steps of the S product
+  constexpr int DB = D / 32;             // 32-wide d blocks of the output
+  constexpr float kLazy = 8.f;           // rescale only when the running max grows by > 2^8
+  __shared__ __align__(16) uint16_t k_lds0[kKeyChunk * D];   // [64 keys][D], MFMA row order
+  __shared__ __align__(16) uint16_t k_lds1[kKeyChunk * D];
+  __shared__ __align__(16) uint16_t v_lds0[kKeyChunk * D];   // [64 keys][D], key order
+  __shared__ __align__(16) uint16_t v_lds1[kKeyChunk * D];
+  __shared__ int s_item;
+
+  const int Hq = Hkv * G;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int grp = wave < 4 ? 0 : 1;
+  const int lane = threadIdx.x % kWave;
+  const int n = lane & 31;
+  const int g = lane >> 5;
+  const int xcd = blockIdx.x % kNumXcd;
+  const int nitems = ws.ctrl[0] * Hkv;
+  const int tq = lane >> 4;
+  const int ti = lane & 15;
+  const int v_row_off = 8 * (tq >> 1) + (ti >> 2);
+  const int v_d_off = 16 * (tq & 1) + 4 * (ti & 3);
+  const uint32_t row_bytes = static_cast<uint32_t>(Hkv) * D * 2;
+  const uint32_t koff_lane = dma_lane_off<D, false>(lane, row_bytes);
+  const uint32_t voff_lane = dma_lane_off<D, true>(lane, row_bytes);
+  __builtin_assume(wave < G);
+
+  for (;;) {
+    if (threadIdx.x == 0) s_item = atomicAdd(&ws.ctrl[8 + xcd], 1) * kNumXcd + xcd;
+    __syncthreads();
+    const int item = __builtin_amdgcn_readfirstlane(s_item);
+    __syncthreads();
+    if (item >= nitems) break;
+    const int slot = ws.order[item / Hkv];
+    const int kvh = item % Hkv;
+    TileDesc t = ws.tiles[slot];
+    t.req = __builtin_amdgcn_readfirstlane(t.req);
+    t.p0 = __builtin_amdgcn_readfirstlane(t.p0);
+    t.nrows = __builtin_amdgcn_readfirstlane(t.nrows);
+    t.npre = __builtin_amdgcn_readfirstlane(t.npre);
+    t.seg_start = __builtin_amdgcn_readfirstlane(t.seg_start);
+    t.seg_len = __builtin_amdgcn_readfirstlane(t.seg_len);
+    t.ndiag = __builtin_amdgcn_readfirstlane(t.ndiag);
+    const int base = rows.seg_row0[t.req];
+    const int64_t pbase = rows.pre_row0 != nullptr ? rows.pre_row0[t.req] : static_cast<int64_t>(base);
+    const int h = kvh * G + wave;
+    const int nv = tile_key_count(t);
+    const int nF = nv - t.ndiag;
+    const int npre = t.npre;
+    const int seg_shift = t.seg_start - npre;
+    const size_t tok_stride = static_cast<size_t>(Hkv) * D;
+    const size_t head0 = static_cast<size_t>(base) * tok_stride + static_cast<size_t>(kvh) * D;
+    const size_t phead0 = static_cast<size_t>(pbase) * tok_stride + static_cast<size_t>(kvh) * D;
+    const char *kreq = uniform_ptr(reinterpret_cast<const char *>(rows.seg_k + head0));
+    const char *vreq = uniform_ptr(reinterpret_cast<const char *>(rows.seg_v + head0));
+    const char *kpre = uniform_ptr(reinterpret_cast<const char *>(rows.pre_k + phead0));
+    const char *vpre = uniform_ptr(reinterpret_cast<const char *>(rows.pre_v + phead0));
+    const int nch = (nv + kKeyChunk - 1) / kKeyChunk;
+
+    bf16x8 qf[DS];
+    {
+      const bool ok = n < t.nrows;
+      const uint16_t *qrow = q + (static_cast<size_t>(base + t.p0 + n) * Hq + h) * D;
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) {
+        u32x4 w = {0u, 0u, 0u, 0u};
+        if (ok) w = *reinterpret_cast<const u32x4 *>(qrow + 16 * ds + 8 * g);
+        qf[ds] = __builtin_bit_cast(bf16x8, w);
+      }
+    }
+    f32x16 oacc[DB];
+#pragma unroll
+    for (int i = 0; i < DB; ++i) oacc[i] = f32x16{};
+    float m_run = -INFINITY;
+    float l_run = 0.f;
+    f32x16 sacc[2];       // S(c), from the matrix phase to the softmax phase
+    bf16x8 pb[4];         // P(c) in bf16, from the softmax phase to the next matrix phase
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) sacc[kb] = f32x16{};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pb[i] = bf16x8{};
+
+    // matrix phase c: O += V(c-1)^T . P(c-1)^T, then S(c) = K(c) . Q^T (both from slot c % 2)
+    auto matrix_phase = [&](int c, const uint16_t *kc_lds, const uint16_t *vc_lds) {
+      if (c >= 1) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const int dd = db * 32 + v_d_off;
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks) {
+            v4i16 part[2];
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+              const int r = 16 * ks + 4 * hh + v_row_off;
+              const int chunk = (dd >> 3) ^ swz_v<D>(r);
+              const uint16_t *pa = &vc_lds[r * D + chunk * 8 + (dd & 4)];
+              part[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)pa);
+            }
+            const u32x4 w = {__builtin_bit_cast(uint2, part[0]).x, __builtin_bit_cast(uint2, part[0]).y,
+                             __builtin_bit_cast(uint2, part[1]).x, __builtin_bit_cast(uint2, part[1]).y};
+            oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w), pb[ks], oacc[db], 0,
+                                                               0, 0);
+          }
+        }
+      }
+      if (c < nch) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          sacc[kb] = f32x16{};
+          const int m = kb * 32 + n;
+#pragma unroll
+          for (int ds = 0; ds < DS; ++ds) {
+            const bf16x8 a =
+                *reinterpret_cast<const bf16x8 *>(&kc_lds[(m * DC + ((2 * ds + g) ^ swz_k<D>(m))) * 8]);
+            sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ds], sacc[kb], 0, 0, 0);
+          }
+        }
+      }
+    };
+    // softmax phase c: mask, lazy max, P(c) in bf16 and the sum of its rounded values
+    auto softmax_phase = [&](int c) {
+      const int vk0 = c * kKeyChunk;
+      if (vk0 + kKeyChunk > nF) {
+        const int lim = min(nv, nF + n + 1) - vk0;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) sacc[kb][e] = (kb * 32 + acc_key(e, g) < lim) ? sacc[kb][e] : -INFINITY;
+      }
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) mloc = fmaxf(mloc, sacc[kb][e]);
+      mloc = pair32_max(mloc) * scale_log2;
+      if (__any(mloc > m_run + kLazy)) {
+        const float m_new = fmaxf(m_run, mloc);
+        const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+        l_run *= corr;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) oacc[db] *= corr;
+      }
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        f32x8 lo, hi;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          lo[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][e], scale_log2, -m_run));
+          hi[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][8 + e], scale_log2, -m_run));
+        }
+        pb[2 * kb] = __builtin_convertvector(lo, bf16x8);
+        pb[2 * kb + 1] = __builtin_convertvector(hi, bf16x8);
+      }
+      l_run += rounded_sum(pb);
+    };
+    // Step c of a group: its matrix phase, a barrier, its softmax phase.  Both groups run
+    // the same code; the second enters one barrier later (and the first leaves one
+    // barrier later), so its step c falls on phases 2c+1 and 2c+2.  Slot c % 2 =
+    // (k_cur, v_cur) holds K(c) and V(c-1).  Only the first group loads: at the start of
+    // its step c it waits for its loads of slot c % 2, passes the barrier, then requests
+    // K(c+1) and V(c) into the other slot, whose last reader (the second group's step
+    // c-1 matrix phase) has passed that barrier too.  Steps run to c = nch, whose
+    // matrix phase only adds P(nch-1).
+    auto pp_step = [&](int c, const uint16_t *k_cur, const uint16_t *v_cur, uint16_t *k_nxt, uint16_t *v_nxt) {
+      wait_vm<0>();
+      lds_barrier();
+      if (grp == 0) {
+        if (c + 1 < nch)
+          stage_tensor<D, 4, false>(k_nxt, kpre, kreq, row_bytes, koff_lane, wave, lane, c + 1, nv, npre, seg_shift);
+        if (c < nch)
+          stage_tensor<D, 4, true>(v_nxt, vpre, vreq, row_bytes, voff_lane, wave, lane, c, nv, npre, seg_shift);
+      }
+      matrix_phase(c, k_cur, v_cur);
+      lds_barrier();
+      if (c < nch) softmax_phase(c);
+    };
+
+    if (grp == 0)
+      stage_tensor<D, 4, false>(k_lds0, kpre, kreq, row_bytes, koff_lane, wave, lane, 0, nv, npre, seg_shift);
+    else
+      lds_barrier();
+    for (int c = 0; c <= nch; c += 2) {
+      pp_step(c, k_lds0, v_lds0, k_lds1, v_lds1);
+      if (c + 1 > nch) break;
+      pp_step(c + 1, k_lds1, v_lds1, k_lds0, v_lds0);
+    }
+    if (grp == 0) lds_barrier();
+
+    const float l_tot = pair32_add(l_run);
+    const float inv = 1.f / l_tot;
+    if (n < t.nrows) {
+      float *orow = out + (static_cast<size_t>(base + t.p0 + n) * Hq + h) * D;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          f32x4 o = {oacc[db][4 * i] * inv, oacc[db][4 * i + 1] * inv, oacc[db][4 * i + 2] * inv,
+                     oacc[db][4 * i + 3] * inv};
+          *reinterpret_cast<f32x4 *>(orow + db * 32 + 8 * i + 4 * g) = o;
+        }
+      }
+    }
+  }
+}
+
 template <int D, int G>
 static hipError_t launch_prefill_dg(int grid, bool stats, int ks, AttnRows rows, PrefillWs ws, int Hkv,
                                     float scale_log2, hipStream_t stream) {
@@ -480,7 +707,9 @@ static hipError_t launch_prefill_dg(int grid, bool stats, int ks, AttnRows rows,
       prefill_kernel<D, G, false, 2><<<dim3(grid), dim3(2 * G * kWave), 0, stream>>>(rows, ws, Hkv, scale_log2);
     else
       return hipErrorInvalidValue;
-  } else
+  } else if constexpr (G > 4)
+    prefill_pp_kernel<D, G><<<dim3(grid), dim3(G * kWave), 0, stream>>>(rows, ws, Hkv, scale_log2);
+  else
     prefill_kernel<D, G, false, 1><<<dim3(grid), dim3(G * kWave), 0, stream>>>(rows, ws, Hkv, scale_log2);
   return hipGetLastError();
 }
@@ -495,7 +724,10 @@ static hipError_t occupancy_dg(bool stats, int ks, int *blocks) {
     else
       return hipErrorInvalidValue;
   }
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, prefill_kernel<D, G, false, 1>, G * kWave, 0);
+  if constexpr (G > 4)
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, prefill_pp_kernel<D, G>, G * kWave, 0);
+  else
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, prefill_kernel<D, G, false, 1>, G * kWave, 0);
 }
 
 #define SONIC_FOR_G(D, X) \
