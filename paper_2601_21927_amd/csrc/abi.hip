@@ -538,8 +538,11 @@ static size_t decode_ws_bytes(int32_t batch, int32_t Hq, int32_t d, int32_t nspl
 
 size_t sonic_decode_workspace_bytes(int32_t batch, int32_t Hq, int32_t d, int32_t max_ctx) {
   if (batch <= 0 || Hq <= 0 || max_ctx <= 0) return 256;
-  // enough for any kv-head count: one kv-head gives the most splits
-  return align_up(decode_ws_bytes(batch, Hq, d, decode_splits(batch, 1, max_ctx)), 256);
+  // enough for any kv-head count the call may use (Hkv dividing Hq, Hq / Hkv <= 8)
+  int nsplit = 1;
+  for (int hkv = 1; hkv <= Hq; ++hkv)
+    if (Hq % hkv == 0 && Hq / hkv <= 8) nsplit = std::max(nsplit, decode_splits(batch, hkv, max_ctx));
+  return align_up(decode_ws_bytes(batch, Hq, d, nsplit), 256);
 }
 
 // Argument checks shared by the two decode entry points.  Returns SONIC_OK with *empty set

@@ -404,16 +404,21 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
   }
 }
 
-// Splits per (request, kv-head): about 256 workgroups (one per CU), each of at
-// least 256 rows.  With that many pairs already, one split, or two when the
-// longest context reaches 2048 rows (so that the longest pair does not outlast
-// the rest of the call when lengths are uneven).
+// Splits per (request, kv-head).  With fewer than 256 pairs, about 256 workgroups,
+// each of at least 256 rows, and at most 8 splits: the merging split loads the
+// partials eight at a time, so a ninth costs it another memory round trip (on the
+// long-dialogue shape, 16 pairs of ~8k rows, 8 splits take 18.1 us per call, 16
+// take 19.3).  With 256 pairs or more, one split, or three when the longest context
+// reaches 2048 rows, so that the longest pairs do not outlast the rest of the call
+// when lengths are uneven (dynamic-budget batch: 1 split 127.7 us, 2 117.1, 3 111.4,
+// 4 121.3 per call).
 int decode_splits(int batch, int Hkv, int max_ctx) {
   const long pairs = static_cast<long>(batch) * Hkv;
-  if (pairs >= 256) return max_ctx >= 2048 ? 2 : 1;
+  if (pairs >= 256) return max_ctx >= 2048 ? 3 : 1;
   long s = (256 + pairs - 1) / pairs;
   const long by_rows = (static_cast<long>(max_ctx) + 255) / 256;
   if (s > by_rows) s = by_rows;
+  if (s > 8) s = 8;
   return static_cast<int>(s < 1 ? 1 : s);
 }
 

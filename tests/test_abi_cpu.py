@@ -132,6 +132,9 @@ def test_workspace_sizes():
     assert sonic.prefill_workspace_bytes(1, 10, 4, 0, 64) == 0
     assert sonic.prefill_workspace_bytes(1, 10, 0, 2, 64) == 0
     assert sonic.decode_workspace_bytes(8, 32, 128, 1584) >= 8 * 32 * 130 * 4
+    # enough for every kv-head count dividing Hq: with 128 requests and 2 kv-heads there are 256
+    # (request, kv-head) pairs, which take three splits at contexts of 2048 rows and more
+    assert sonic.decode_workspace_bytes(128, 8, 128, 4096) >= 128 * 8 * 3 * 130 * 4
 
 
 def test_softmax_scale_argument_checks_without_gpu():
