@@ -501,7 +501,8 @@ def widened_rows(P, timer):
     ext_k, ext_v = cache.k.clone(), cache.v.clone()
     eq, ek, e_v = (bf16_to_device(x[allpos], dev) for x in (b.q, b.k, b.v))
     ext_out = torch.empty((len(allpos), Hq, d), dtype=torch.float32, device=dev)
-    ext_ws = torch.empty(max(sonic.nexus_extend_workspace_bytes(B, len(allpos)), 256), dtype=torch.uint8, device=dev)
+    ext_ws = torch.empty(max(sonic.nexus_extend_workspace_bytes(B, len(allpos), P.max_ctx, Hkv, d), 256),
+                         dtype=torch.uint8, device=dev)
 
     def run_extend():
         P.ok(sonic.nexus_extend(ext_cu, ext_keep, ext_k, ext_v, cache.row_off, cache.row_cap, ext_len, eq, ek,

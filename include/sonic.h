@@ -13,10 +13,11 @@
  *                                 Sec. 3.2 after Eq.(4); App. C);
  *   sonic_compressed_decode     - one generation step over the retained context
  *                                 {I_sys, N, Q_n} (App. C, Eq.(15));
- *   sonic_nexus_extend          - when a turn ends, its Nexus tokens over the
- *                                 compact cache, then the turn's rows replaced
- *                                 by their Nexus KV (Sec. 3.2; the Nexus KV is
- *                                 kept for the rest of the session).
+ *   sonic_nexus_extend          - when a turn ends, the Nexus tokens of its
+ *                                 segments (utterance, response) over the
+ *                                 compact cache, each segment's rows replaced by
+ *                                 its Nexus KV (Sec. 3.2; the Nexus KV is kept
+ *                                 for the rest of the session).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -367,23 +368,33 @@ int32_t sonic_compressed_decode_noalloc(int32_t batch, int32_t num_q_heads, int3
 /* Next turn: the ended turn's Nexus tokens over the compact cache            */
 /* ------------------------------------------------------------------------ */
 
-/* Bytes of device workspace sonic_nexus_extend needs (0 for negative sizes). */
-size_t sonic_nexus_extend_workspace_bytes(int32_t batch, int32_t total_new);
+/*
+ * Bytes of device workspace sonic_nexus_extend needs (0 for negative sizes or
+ * non-positive heads / head_dim): the plan, and room to stage up to max_rows rows of
+ * K and V per request (the tail rows after a segment body, see body_len).
+ */
+size_t sonic_nexus_extend_workspace_bytes(int32_t batch, int32_t total_new, int32_t max_rows,
+                                          int32_t num_kv_heads, int32_t head_dim);
 
 /*
  * When turn n of request b ends, its rows (query and generated response) are the
- * last rows of the request's compact cache, rows keep_len[b] .. cache_len[b]-1;
- * they become the body of a new history segment, followed by that segment's
- * Nexus tokens (Eq.(1)).  For every new Nexus row p and q-head h
+ * last rows of the request's compact cache, rows keep_len[b] .. cache_len[b]-1.  Each
+ * user utterance and each assistant response is a history segment of its own, with
+ * its own Nexus tokens (Eq.(1), Sec. 3.1); one call computes the Nexus tokens of one
+ * segment per request, whose body is the first body_len[b] of those rows (all of
+ * them when body_len is NULL).  For every new Nexus row p and q-head h
  *     out[p][h] = softmax_q(scale * <q[p][h], k[q][g(h)]>) v[q][g(h)]
- * over q in {the request's cache rows 0 .. cache_len[b]-1} u {its new Nexus rows}:
- * by Sec. 3.2 a Nexus row of the newest segment sees the system prompt and the
- * earlier segments' Nexus tokens (Eq.(3)), its own body (Eq.(4)) and all the
- * Nexus tokens of its segment (Eq.(5)), which are exactly these rows.  The
- * result does not depend on whether Nexus tokens see later segments' Nexus
- * tokens, since none exist yet.  Then the new Nexus K/V are written to cache
- * rows keep_len[b] .. over the turn's body, which no later row may see (Eq.(4)),
- * and cache_len[b] becomes keep_len[b] + (number of new Nexus rows of b).
+ * over q in {the request's cache rows 0 .. keep_len[b] + body_len[b] - 1} u {its new
+ * Nexus rows}: by Sec. 3.2 a Nexus row of the segment sees the system prompt and the
+ * earlier segments' Nexus tokens (Eq.(3)), its own body (Eq.(4)) and all the Nexus
+ * tokens of its segment (Eq.(5)), and not the tail rows after the body, which come
+ * later (Eq.(3)).  The result does not depend on whether Nexus tokens see later
+ * segments' Nexus tokens, since none exist yet: utterance then response, one call
+ * each, give what a full prefill with SONIC_NEXUS_UP_TO_OWN gives for both.  Then
+ * the new Nexus K/V are written to cache rows keep_len[b] .., over the body, which no
+ * later row may see (Eq.(4)); the tail rows after the body follow them unchanged; and
+ * cache_len[b] becomes keep_len[b] + (new Nexus rows of b) + (tail rows after the
+ * body).  The next segment's call then takes keep_len[b] + (new Nexus rows of b).
  *
  *   batch, total_new   B and N = nexus_cu[B] (host values); a request may have
  *                      no new Nexus rows (its body is then only dropped)
@@ -392,20 +403,24 @@ size_t sonic_nexus_extend_workspace_bytes(int32_t batch, int32_t total_new);
  *                      request b's new Nexus rows are rows nexus_cu[b] .. of q/k/v
  *   keep_len           device int32 [B]: cache rows kept (system prompt and the
  *                      earlier Nexus tokens), 0 <= keep_len[b] <= cache_len[b]
+ *   body_len           NULL, or device int32 [B]: rows of the segment's body,
+ *                      0 <= body_len[b] <= cache_len[b] - keep_len[b]
  *   k_cache .. cache_len   the compact cache, as for sonic_compressed_decode
  *   q                  device bf16 [N][Hq][d];  k, v: device bf16 [N][Hkv][d]
+ *   softmax_scale      0 for 1/sqrt(d), else finite and > 0
  *   out                device fp32 [N][Hq][d]
- *   workspace          device, 256-byte aligned, >= sonic_nexus_extend_workspace_bytes(B, N);
+ *   workspace          device, 256-byte aligned,
+ *                      >= sonic_nexus_extend_workspace_bytes(B, N, max_rows, Hkv, d);
  *                      contents need no initialisation
  *   dev_status         SONIC_ERR_BAD_LAYOUT when nexus_cu or the lengths are
- *                      inconsistent, SONIC_ERR_CAPACITY when keep_len[b] plus the new
- *                      rows exceed the capacity; then (as with any pending status)
+ *                      inconsistent, SONIC_ERR_CAPACITY when the new length would
+ *                      exceed the capacity; then (as with any pending status)
  *                      nothing is written
  * Returns SONIC_ERR_UNSUPPORTED when max_rows or N rows of one tensor reach 4 GiB.
  */
 int32_t sonic_nexus_extend(int32_t batch, int32_t total_new, int32_t num_q_heads, int32_t num_kv_heads,
                            int32_t head_dim, int32_t max_rows, const int32_t *nexus_cu, const int32_t *keep_len,
-                           void *k_cache, void *v_cache, const int64_t *cache_row_off,
+                           const int32_t *body_len, void *k_cache, void *v_cache, const int64_t *cache_row_off,
                            const int32_t *cache_row_cap, int32_t *cache_len, const void *q, const void *k,
                            const void *v, float softmax_scale, float *out, void *workspace,
                            size_t workspace_bytes, int32_t *dev_status, void *stream);

@@ -24,12 +24,17 @@ hipError_t launch_key_weight(int batch, int T, int Hq, int Hkv, int D, int num_c
                              const uint8_t *role, const uint16_t *q, const uint16_t *k, PrefillWs ws,
                              float scale_log2, float *w, int32_t *status, hipStream_t stream);
 hipError_t launch_plan_extend(int batch, int total_new, int max_rows, const int32_t *nexus_cu,
-                              const int32_t *keep_len, const int32_t *cache_len, const int32_t *row_cap,
-                              PrefillWs ws, int32_t *status, hipStream_t stream);
-hipError_t launch_extend_append(int batch, int max_new, int Hkv, int D, const int32_t *nexus_cu,
+                              const int32_t *keep_len, const int32_t *body_len, const int32_t *cache_len,
+                              const int32_t *row_cap, PrefillWs ws, int32_t *status, hipStream_t stream);
+hipError_t launch_extend_stage(int batch, int max_rows, int Hkv, int D, const int32_t *keep_len,
+                               const int32_t *body_len, const uint16_t *kc, const uint16_t *vc, const int64_t *row_off,
+                               PrefillWs ws, uint16_t *k_stage, uint16_t *v_stage, const int32_t *status,
+                               hipStream_t stream);
+hipError_t launch_extend_append(int batch, int max_new, int max_rows, int Hkv, int D, const int32_t *nexus_cu,
                                 const int32_t *keep_len, uint16_t *kc, uint16_t *vc, const int64_t *row_off,
-                                int32_t *cache_len, const uint16_t *k_new, const uint16_t *v_new,
-                                const int32_t *status, hipStream_t stream);
+                                int32_t *cache_len, const uint16_t *k_new, const uint16_t *v_new, PrefillWs ws,
+                                const uint16_t *k_stage, const uint16_t *v_stage, const int32_t *status,
+                                hipStream_t stream);
 hipError_t launch_prefill(int D, int G, int grid, bool stats, int ks, AttnRows rows, PrefillWs ws, int Hkv, float scale_log2,
                           hipStream_t stream);
 hipError_t launch_compact(int batch, int total_tokens, int max_seqlen, int Hkv, int D, const int32_t *cu,
@@ -48,7 +53,7 @@ hipError_t launch_decode(int batch, int Hq, int Hkv, int D, int max_ctx, int nsp
 
 namespace {
 
-constexpr int kAbiVersion = 9;
+constexpr int kAbiVersion = 10;
 constexpr double kLog2e = 1.4426950408889634;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -318,7 +323,10 @@ int32_t sonic_segment_attn_prefill(int32_t batch, int32_t total_tokens, int32_t 
 }
 
 // ---------------------------------------------------------------- next-turn Nexus step
-static size_t extend_ws_layout(int32_t batch, int32_t total_new, PrefillWs *ws, char *base) {
+// Workspace: the plan (per request, per new row), then the staging rows for the tail
+// rows after a segment body (max_rows per request, K and V).
+static size_t extend_ws_layout(int32_t batch, int32_t total_new, int32_t max_rows, size_t row_bytes, PrefillWs *ws,
+                               uint16_t **k_stage, uint16_t **v_stage, char *base) {
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -331,26 +339,33 @@ static size_t extend_ws_layout(int32_t batch, int32_t total_new, PrefillWs *ws, 
   char *tiles = take(sizeof(TileDesc) * N1);
   char *order = take(sizeof(int32_t) * N1);
   char *ctrl = take(sizeof(int32_t) * 16);
+  const size_t stage_bytes = B1 * static_cast<size_t>(max_rows > 0 ? max_rows : 1) * row_bytes;
+  char *ks = take(stage_bytes);
+  char *vs = take(stage_bytes);
   if (ws) {
     *ws = PrefillWs{};
     ws->req = reinterpret_cast<ReqInfo *>(req);
     ws->tiles = reinterpret_cast<TileDesc *>(tiles);
     ws->order = reinterpret_cast<int32_t *>(order);
     ws->ctrl = reinterpret_cast<int32_t *>(ctrl);
+    *k_stage = reinterpret_cast<uint16_t *>(ks);
+    *v_stage = reinterpret_cast<uint16_t *>(vs);
   }
   return off;
 }
 
-size_t sonic_nexus_extend_workspace_bytes(int32_t batch, int32_t total_new) {
-  if (batch < 0 || total_new < 0) return 0;
-  return extend_ws_layout(batch, total_new, nullptr, nullptr);
+size_t sonic_nexus_extend_workspace_bytes(int32_t batch, int32_t total_new, int32_t max_rows, int32_t num_kv_heads,
+                                          int32_t head_dim) {
+  if (batch < 0 || total_new < 0 || max_rows < 0 || num_kv_heads <= 0 || head_dim <= 0) return 0;
+  return extend_ws_layout(batch, total_new, max_rows, static_cast<size_t>(num_kv_heads) * head_dim * 2, nullptr,
+                          nullptr, nullptr, nullptr);
 }
 
 int32_t sonic_nexus_extend(int32_t batch, int32_t total_new, int32_t Hq, int32_t Hkv, int32_t d, int32_t max_rows,
-                           const int32_t *nexus_cu, const int32_t *keep_len, void *k_cache, void *v_cache,
-                           const int64_t *cache_row_off, const int32_t *cache_row_cap, int32_t *cache_len,
-                           const void *q, const void *k, const void *v, float softmax_scale, float *out,
-                           void *workspace, size_t workspace_bytes, int32_t *dev_status, void *stream_) {
+                           const int32_t *nexus_cu, const int32_t *keep_len, const int32_t *body_len, void *k_cache,
+                           void *v_cache, const int64_t *cache_row_off, const int32_t *cache_row_cap,
+                           int32_t *cache_len, const void *q, const void *k, const void *v, float softmax_scale,
+                           float *out, void *workspace, size_t workspace_bytes, int32_t *dev_status, void *stream_) {
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   if (batch < 0 || total_new < 0 || Hq <= 0 || Hkv <= 0 || max_rows < 0 || dev_status == nullptr)
     return SONIC_ERR_INVALID_ARG;
@@ -374,14 +389,23 @@ int32_t sonic_nexus_extend(int32_t batch, int32_t total_new, int32_t Hq, int32_t
       static_cast<size_t>(total_new) * row_bytes >= (size_t(1) << 32))
     return SONIC_ERR_UNSUPPORTED;
   PrefillWs ws;
-  const size_t need = extend_ws_layout(batch, total_new, &ws, static_cast<char *>(workspace));
+  uint16_t *k_stage = nullptr, *v_stage = nullptr;
+  const size_t need = extend_ws_layout(batch, total_new, max_rows, row_bytes, &ws, &k_stage, &v_stage,
+                                       static_cast<char *>(workspace));
   if (workspace_bytes < need) return SONIC_ERR_WORKSPACE;
   DeviceInfo *di = nullptr;
   hipError_t e = device_info(&di);
   if (e != hipSuccess) return SONIC_ERR_HIP;
-  e = launch_plan_extend(batch, total_new, max_rows, nexus_cu, keep_len, cache_len, cache_row_cap, ws, dev_status,
-                         stream);
+  e = launch_plan_extend(batch, total_new, max_rows, nexus_cu, keep_len, body_len, cache_len, cache_row_cap, ws,
+                         dev_status, stream);
   if (e != hipSuccess) return SONIC_ERR_HIP;
+  if (body_len != nullptr) {
+    // the tail rows after the body, staged before the cache update moves them
+    e = launch_extend_stage(batch, max_rows, Hkv, d, keep_len, body_len, static_cast<const uint16_t *>(k_cache),
+                            static_cast<const uint16_t *>(v_cache), cache_row_off, ws, k_stage, v_stage, dev_status,
+                            stream);
+    if (e != hipSuccess) return SONIC_ERR_HIP;
+  }
   if (total_new > 0) {
     // Fewer work items than twice the CUs (the usual next turn: a few blocks of new
     // rows per request) would leave CUs idle: split each item's keys over two wave
@@ -396,9 +420,11 @@ int32_t sonic_nexus_extend(int32_t batch, int32_t total_new, int32_t Hq, int32_t
     e = launch_prefill(d, G, grid, false, ks, rows, ws, Hkv, static_cast<float>(softmax_scale * kLog2e), stream);
     if (e != hipSuccess) return SONIC_ERR_HIP;
   }
-  e = launch_extend_append(batch, total_new, Hkv, d, nexus_cu, keep_len, static_cast<uint16_t *>(k_cache),
+  e = launch_extend_append(batch, total_new, max_rows, Hkv, d, nexus_cu, keep_len, static_cast<uint16_t *>(k_cache),
                            static_cast<uint16_t *>(v_cache), cache_row_off, cache_len,
-                           static_cast<const uint16_t *>(k), static_cast<const uint16_t *>(v), dev_status, stream);
+                           static_cast<const uint16_t *>(k), static_cast<const uint16_t *>(v), ws,
+                           body_len != nullptr ? k_stage : nullptr, body_len != nullptr ? v_stage : nullptr,
+                           dev_status, stream);
   return finish(e, dev_status, stream);
 }
 

@@ -160,7 +160,7 @@ struct ReqInfo {
   int32_t ntiles;
   int32_t system;
   int32_t nexus_total;
-  int32_t nruns;
+  int32_t nruns;       // runs of the request (the next-turn plan: tail rows after the segment body)
   int64_t cost;        // sum of tile_cost over the request's descriptors
   int64_t pad;
 };

@@ -80,9 +80,9 @@ def lib() -> ctypes.CDLL:
     L.sonic_compressed_decode_noalloc.argtypes = [_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p,
                                                   _f32, _p, _p, _p]
     L.sonic_nexus_extend_workspace_bytes.restype = _sz
-    L.sonic_nexus_extend_workspace_bytes.argtypes = [_i32, _i32]
+    L.sonic_nexus_extend_workspace_bytes.argtypes = [_i32, _i32, _i32, _i32, _i32]
     L.sonic_nexus_extend.restype = _i32
-    L.sonic_nexus_extend.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p,
+    L.sonic_nexus_extend.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p,
                                      _f32, _p, _p, _sz, _p, _p]
     L.sonic_role_projection_workspace_bytes.restype = _sz
     L.sonic_role_projection_workspace_bytes.argtypes = [_i32]
@@ -243,25 +243,28 @@ def compressed_decode_noalloc(k_cache, v_cache, cache_row_off, cache_row_cap, ca
 
 
 # ----------------------------------------------------------------- next turn: Nexus step
-def nexus_extend_workspace_bytes(batch: int, total_new: int) -> int:
-    return int(lib().sonic_nexus_extend_workspace_bytes(batch, total_new))
+def nexus_extend_workspace_bytes(batch: int, total_new: int, max_rows: int, num_kv_heads: int,
+                                 head_dim: int) -> int:
+    return int(lib().sonic_nexus_extend_workspace_bytes(batch, total_new, max_rows, num_kv_heads, head_dim))
 
 
 def nexus_extend(nexus_cu, keep_len, k_cache, v_cache, cache_row_off, cache_row_cap, cache_len, q, k, v, out,
-                 workspace, dev_status, max_rows: int, softmax_scale=None, stream=None) -> int:
-    """nexus_cu int32 [B+1]; keep_len int32 [B]; q [N,Hq,d] bf16; k/v [N,Hkv,d] bf16; out [N,Hq,d] fp32."""
-    _dev(nexus_cu, keep_len, k_cache, v_cache, cache_row_off, cache_row_cap, cache_len, q, k, v, out, workspace,
-         dev_status)
-    _types(nexus_cu=(nexus_cu, _I32), keep_len=(keep_len, _I32), k_cache=(k_cache, _BF16), v_cache=(v_cache, _BF16),
-           cache_row_off=(cache_row_off, _I64), cache_row_cap=(cache_row_cap, _I32), cache_len=(cache_len, _I32),
-           q=(q, _BF16), k=(k, _BF16), v=(v, _BF16), out=(out, _F32), dev_status=(dev_status, _I32))
+                 workspace, dev_status, max_rows: int, body_len=None, softmax_scale=None, stream=None) -> int:
+    """nexus_cu int32 [B+1]; keep_len int32 [B]; body_len int32 [B] or None (the whole tail);
+    q [N,Hq,d] bf16; k/v [N,Hkv,d] bf16; out [N,Hq,d] fp32."""
+    _dev(nexus_cu, keep_len, body_len, k_cache, v_cache, cache_row_off, cache_row_cap, cache_len, q, k, v, out,
+         workspace, dev_status)
+    _types(nexus_cu=(nexus_cu, _I32), keep_len=(keep_len, _I32), body_len=(body_len, _I32),
+           k_cache=(k_cache, _BF16), v_cache=(v_cache, _BF16), cache_row_off=(cache_row_off, _I64),
+           cache_row_cap=(cache_row_cap, _I32), cache_len=(cache_len, _I32), q=(q, _BF16), k=(k, _BF16),
+           v=(v, _BF16), out=(out, _F32), dev_status=(dev_status, _I32))
     N, Hq, d = q.shape
     Hkv = k.shape[1]
     scale = 0.0 if softmax_scale is None else float(softmax_scale)   # 0: the library's 1/sqrt(d)
     return int(lib().sonic_nexus_extend(
-        nexus_cu.numel() - 1, N, Hq, Hkv, d, int(max_rows), _ptr(nexus_cu), _ptr(keep_len), _ptr(k_cache),
-        _ptr(v_cache), _ptr(cache_row_off), _ptr(cache_row_cap), _ptr(cache_len), _ptr(q), _ptr(k), _ptr(v), scale,
-        _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(dev_status),
+        nexus_cu.numel() - 1, N, Hq, Hkv, d, int(max_rows), _ptr(nexus_cu), _ptr(keep_len), _ptr(body_len),
+        _ptr(k_cache), _ptr(v_cache), _ptr(cache_row_off), _ptr(cache_row_cap), _ptr(cache_len), _ptr(q), _ptr(k),
+        _ptr(v), scale, _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(dev_status),
         _stream(stream)))
 
 

@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert sonic.abi_version() == 9
+    assert sonic.abi_version() == 10
     assert sonic.status_string(0) == "ok"
     for code in range(1, 7):
         assert sonic.status_string(code) != "unknown status"
@@ -152,7 +152,7 @@ def test_softmax_scale_argument_checks_without_gpu():
         return L.sonic_compressed_decode(0, 4, 2, 64, 16, n, n, n, n, n, n, n, n, n, scale, n, n, 0, sp, n)
 
     def extend(scale):
-        return L.sonic_nexus_extend(0, 0, 4, 2, 64, 16, n, n, n, n, n, n, n, n, n, n, scale, n, n, 0, sp, n)
+        return L.sonic_nexus_extend(0, 0, 4, 2, 64, 16, n, n, n, n, n, n, n, n, n, n, n, scale, n, n, 0, sp, n)
 
     for call in (prefill, decode, extend):
         assert call(0.0) == sonic.OK

@@ -57,8 +57,8 @@ class ExtendCase:
         self.k = bf16_to_device(batch.k[allpos])
         self.v = bf16_to_device(batch.v[allpos])
         self.out = torch.full((len(allpos), batch.num_q_heads, d), 7.0, dtype=torch.float32, device="cuda")
-        self.ws = torch.empty(max(sonic.nexus_extend_workspace_bytes(B, len(allpos)), 256), dtype=torch.uint8,
-                              device="cuda")
+        self.ws = torch.empty(max(sonic.nexus_extend_workspace_bytes(B, len(allpos), int(self.cap.max()), Hkv, d),
+                                  256), dtype=torch.uint8, device="cuda")
         self.status = torch.zeros(1, dtype=torch.int32, device="cuda")
 
     def run(self):
@@ -222,3 +222,95 @@ def test_extend_many_new_rows():
             W.RequestLayout(17, [30, 612], [5, 598], 0), W.RequestLayout(0, [720], [599], 0)]
     batch = W.make_batch("ext-many", lays, 32, 8, 128, seed=21)
     check_case(ExtendCase(batch), "many rows")
+
+
+def _turn_layouts(rng, n, **kw):
+    out = []
+    while len(out) < n:
+        lay = W.random_layout(rng, max_c=0, **kw)
+        if len(lay.bodies) >= 2:
+            out.append(lay)
+    return out
+
+
+@pytest.mark.parametrize("Hq,Hkv,d", [(4, 2, 64), (28, 4, 128), (32, 8, 128)])
+def test_extend_two_segment_turn(Hq, Hkv, d):
+    """A turn of two segments (utterance, response), one call each with the utterance's body
+    length first: outputs against the oracle's two steps, cache rows and lengths bit for bit
+    after each call."""
+    H.need_gpu()
+    rng = np.random.default_rng(700 + Hq + Hkv + d)
+    lays = _turn_layouts(rng, 4, max_h=5, max_b=150, max_k=60, max_s=80)
+    lays.append(W.RequestLayout(9, [40, 3, 70], [5, 20, 0], 0))    # more Nexus rows than utterance rows
+    batch = W.make_batch("turn", lays, Hq, Hkv, d, seed=int(rng.integers(1 << 30)))
+    B, cu = batch.batch, batch.cu_seqlens
+    pos = [W.turn_positions(l) for l in lays]
+    len0 = np.array([len(p[0]) for p in pos], np.int64)
+    ku = np.array([len(p[3]) for p in pos], np.int64)
+    kr = np.array([len(p[4]) for p in pos], np.int64)
+    keep = np.array([p[1] for p in pos], np.int64)
+    rb = len0 - keep - np.array([p[2] for p in pos])
+    cap = np.maximum(np.maximum(len0, keep + ku + rb), keep + ku + kr) + 3
+    off = np.concatenate([[0], np.cumsum(cap)[:-1]]).astype(np.int64)
+    kc = np.full((int(cap.sum()), Hkv, d), 0x7FC1, np.uint16)
+    vc = kc.copy()
+    for b in range(B):
+        o = int(off[b])
+        kc[o:o + len0[b]] = batch.k[pos[b][0] + int(cu[b])]
+        vc[o:o + len0[b]] = batch.v[pos[b][0] + int(cu[b])]
+    dkc, dvc = bf16_to_device(kc), bf16_to_device(vc)
+    row_off = torch.from_numpy(off).cuda()
+    row_cap = torch.from_numpy(cap.astype(np.int32)).cuda()
+    length = torch.from_numpy(len0.astype(np.int32)).cuda()
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    max_rows = int(cap.max())
+    # oracle state per request: the cache rows as bf16 bits
+    ok = [kc[int(off[b]):int(off[b]) + len0[b]].copy() for b in range(B)]
+    ov = [vc[int(off[b]):int(off[b]) + len0[b]].copy() for b in range(B)]
+    for step, (kn, sel, body) in enumerate(((ku, 3, np.array([p[2] for p in pos])), (kr, 4, None))):
+        kp = keep if step == 0 else keep + ku
+        rows = [pos[b][sel] + int(cu[b]) for b in range(B)]
+        allpos = np.concatenate(rows)
+        ncu = torch.from_numpy(np.concatenate([[0], np.cumsum(kn)]).astype(np.int32)).cuda()
+        out = torch.full((len(allpos), Hq, d), 7.0, dtype=torch.float32, device="cuda")
+        ws = torch.empty(sonic.nexus_extend_workspace_bytes(B, len(allpos), max_rows, Hkv, d), dtype=torch.uint8,
+                         device="cuda")
+        bl = None if body is None else torch.from_numpy(body.astype(np.int32)).cuda()
+        st = sonic.nexus_extend(ncu, torch.from_numpy(kp.astype(np.int32)).cuda(), dkc, dvc, row_off, row_cap, length,
+                                bf16_to_device(batch.q[allpos]), bf16_to_device(batch.k[allpos]),
+                                bf16_to_device(batch.v[allpos]), out, ws, status, max_rows=max_rows, body_len=bl)
+        assert st == sonic.OK
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0, sonic.status_string(int(status.item()))
+        got = out.cpu().numpy()
+        gk, gv, gl = bf16_to_host(dkc), bf16_to_host(dvc), length.cpu().numpy()
+        c = np.concatenate([[0], np.cumsum(kn)])
+        for b in range(B):
+            r = rows[b]
+            want, ok[b], ov[b] = OE.extend_request(batch.q[r], batch.k[r], batch.v[r], ok[b], ov[b], int(kp[b]),
+                                                   body_len=None if body is None else int(body[b]))
+            if len(want):
+                H.assert_close(got[c[b]:c[b + 1]], want, f"turn step {step} request {b}")
+            o = int(off[b])
+            assert gl[b] == len(ok[b]), (step, b, gl[b], len(ok[b]))
+            assert np.array_equal(gk[o:o + len(ok[b])], ok[b]) and np.array_equal(gv[o:o + len(ov[b])], ov[b]), \
+                (step, b)
+
+
+def test_extend_body_longer_than_the_tail_is_a_layout_error():
+    H.need_gpu()
+    rng = np.random.default_rng(41)
+    lays = _ending_layouts(rng, 2, max_h=3, max_b=40, max_k=12, max_s=20)
+    batch = W.make_batch("bodylen", lays, 4, 2, 64, seed=41)
+    case = ExtendCase(batch)
+    tail = case.len0 - np.array(case.keep)
+    bl = torch.from_numpy((tail + np.array([0, 1])).astype(np.int32)).cuda()
+    kc0, len0 = bf16_to_host(case.kc).copy(), case.length.cpu().numpy().copy()
+    st = sonic.nexus_extend(case.nexus_cu, case.keep_len, case.kc, case.vc, case.row_off, case.row_cap, case.length,
+                            case.q, case.k, case.v, case.out, case.ws, case.status, max_rows=int(case.cap.max()),
+                            body_len=bl)
+    assert st == sonic.OK
+    torch.cuda.synchronize()
+    assert int(case.status.item()) == sonic.ERR_BAD_LAYOUT
+    assert np.array_equal(bf16_to_host(case.kc), kc0) and np.array_equal(case.length.cpu().numpy(), len0)
+    assert torch.all(case.out == 7.0)

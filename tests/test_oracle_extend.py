@@ -73,27 +73,6 @@ def test_no_nexus_rows_only_drops_the_body():
     assert out.shape[0] == 0 and np.array_equal(nk, b.k[cache_pos[:keep]])
 
 
-def _turn_positions(lay):
-    """Positions for a turn of two segments (the layout's last two: utterance U, response R):
-    the cache rows before the step (system, earlier Nexus, U body, R body), keep, |U|, and the
-    positions of U's and R's Nexus rows."""
-    h = len(lay.bodies)
-    p = lay.system
-    cache = list(range(lay.system))
-    starts = []
-    for i, (bl, k) in enumerate(zip(lay.bodies, lay.nexus)):
-        starts.append(p)
-        if i < h - 2:
-            cache += list(range(p + bl, p + bl + k))
-        p += bl + k
-    u0, r0 = starts[h - 2], starts[h - 1]
-    cache += list(range(u0, u0 + lay.bodies[h - 2])) + list(range(r0, r0 + lay.bodies[h - 1]))
-    keep = lay.system + sum(lay.nexus[:h - 2])
-    nu = np.arange(u0 + lay.bodies[h - 2], u0 + lay.bodies[h - 2] + lay.nexus[h - 2])
-    nr = np.arange(r0 + lay.bodies[h - 1], r0 + lay.bodies[h - 1] + lay.nexus[h - 1])
-    return np.array(cache, np.int64), keep, lay.bodies[h - 2], nu, nr
-
-
 def _two_segment_layouts(rng, n):
     out = []
     while len(out) < n:
@@ -112,7 +91,7 @@ def test_two_segment_turn_equals_own_and_earlier_scope_prefill(seed):
     rng = np.random.default_rng(1200 + seed)
     for lay in _two_segment_layouts(rng, 3):
         b = W.make_batch("turn", [lay], 4, 2, 32, seed=int(rng.integers(1 << 30)))
-        cache, keep, ulen, nu, nr = _turn_positions(lay)
+        cache, keep, ulen, nu, nr = W.turn_positions(lay)
         out1, k1, v1 = OE.extend_request(b.q[nu], b.k[nu], b.v[nu], b.k[cache], b.v[cache], keep, body_len=ulen)
         out2, k2, v2 = OE.extend_request(b.q[nr], b.k[nr], b.v[nr], k1, v1, keep + len(nu))
         full = OA.prefill_request(b.q, b.k, b.v, b.role, b.turn_id, rows=np.concatenate([nu, nr]),
@@ -132,7 +111,7 @@ def test_two_segment_turn_with_the_whole_tail_as_body_is_caught():
     rng = np.random.default_rng(1290)
     lay = W.RequestLayout(5, [7, 9, 11], [3, 4, 2], 0)
     b = W.make_batch("turn", [lay], 4, 2, 32, seed=5)
-    cache, keep, ulen, nu, nr = _turn_positions(lay)
+    cache, keep, ulen, nu, nr = W.turn_positions(lay)
     full = OA.prefill_request(b.q, b.k, b.v, b.role, b.turn_id, rows=nu, nexus_scope=OM.NEXUS_UP_TO_OWN)
     wrong, _, _ = OE.extend_request(b.q[nu], b.k[nu], b.v[nu], b.k[cache], b.v[cache], keep)
     assert np.abs(wrong - full).max() > 1e-3

@@ -312,6 +312,32 @@ def extend_positions(lay: RequestLayout):
     return np.array(cache, np.int64), keep, np.array(nexus, np.int64)
 
 
+def turn_positions(lay: RequestLayout):
+    """Positions (in the layout) of a turn of two segments, the layout's last two (an
+    utterance U, then a response R): (cache rows in order: system, the earlier segments'
+    Nexus, U's body, R's body; rows kept; U's body length; positions of U's Nexus rows;
+    positions of R's Nexus rows).  The layout must have at least two segments and no
+    current-query tokens."""
+    h = len(lay.bodies)
+    if h < 2 or lay.current:
+        raise ValueError("needs two history segments last and no current query")
+    p = lay.system
+    cache = list(range(lay.system))
+    starts = []
+    for i, (b, k) in enumerate(zip(lay.bodies, lay.nexus)):
+        starts.append(p)
+        if i < h - 2:
+            cache += list(range(p + b, p + b + k))
+        p += b + k
+    u0, r0 = starts[h - 2], starts[h - 1]
+    ub, rb = lay.bodies[h - 2], lay.bodies[h - 1]
+    cache += list(range(u0, u0 + ub)) + list(range(r0, r0 + rb))
+    keep = lay.system + sum(lay.nexus[:h - 2])
+    nu = np.arange(u0 + ub, u0 + ub + lay.nexus[h - 2])
+    nr = np.arange(r0 + rb, r0 + rb + lay.nexus[h - 1])
+    return np.array(cache, np.int64), keep, ub, nu, nr
+
+
 def text_only_layout(lay: RequestLayout) -> RequestLayout:
     """The same conversation without Nexus tokens: what a full-context model keeps."""
     return RequestLayout(lay.system, list(lay.bodies), [0] * len(lay.bodies), lay.current)
