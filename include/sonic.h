@@ -309,7 +309,7 @@ size_t sonic_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t 
  * generated token belongs to the current turn, so it sees every retained row.
  * cache_len[b] is incremented on the device, so a decode loop needs no host
  * round trip.  One kernel: the context of each (request, kv-head) is split over
- * up to min(8, ~256 / (B * Hkv)) workgroups (three for 256 or more pairs with
+ * up to min(16, 256 / (B * Hkv)) workgroups (three for 256 or more pairs with
  * contexts of 2048 rows and more), and the split that finishes last merges the
  * partials by log-sum-exp.
  *

@@ -35,6 +35,7 @@ namespace sonic {
 constexpr int kDecWaves = 8;
 constexpr int kDecThreads = kDecWaves * kWave;
 constexpr int kGroupRows = 16;
+constexpr int kMergeBatch = 16;   // partials loaded per memory round trip of the merge
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
@@ -130,7 +131,7 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
 
   // Every split counts itself once, after its partial (if any) is stored.  The last
   // to count merges the partials of the nsp splits with rows by log-sum-exp, a batch
-  // of eight per memory round trip, writes the output, and counts the pair for its
+  // of kMergeBatch per memory round trip, writes the output, and counts the pair for its
   // request while the partials load; the last pair of a request advances the length.
   auto finish_pair = [&]() {
     if (threadIdx.x == 0) s_last = (atomicAdd(&ws.arrive[pair], 1) == nsplit - 1);
@@ -142,10 +143,10 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
     for (int idx = threadIdx.x; idx < G * D; idx += kDecThreads) {
       const int hh = idx / D, dd = idx % D;
       float M = -INFINITY, L = 0.f, A = 0.f;
-      for (int sp0 = 0; sp0 < nsp; sp0 += 8) {
-        float m[8], l[8], a[8];
+      for (int sp0 = 0; sp0 < nsp; sp0 += kMergeBatch) {
+        float m[kMergeBatch], l[kMergeBatch], a[kMergeBatch];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < kMergeBatch; ++u) {
           const float *r = recs + static_cast<size_t>(min(sp0 + u, nsp - 1)) * REC + hh * (D + 2);
           m[u] = load_sys(r);
           l[u] = load_sys(r + 1);
@@ -153,16 +154,16 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
         }
         wait_vm<0>();
 #pragma unroll
-        for (int u = 0; u < 8; ++u) asm volatile("" : "+v"(m[u]), "+v"(l[u]), "+v"(a[u]));
+        for (int u = 0; u < kMergeBatch; ++u) asm volatile("" : "+v"(m[u]), "+v"(l[u]), "+v"(a[u]));
         float Mb = M;
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
+        for (int u = 0; u < kMergeBatch; ++u)
           if (sp0 + u < nsp) Mb = fmaxf(Mb, m[u]);
         const float c = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mb);
         L *= c;
         A *= c;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < kMergeBatch; ++u) {
           const float w = (sp0 + u < nsp && m[u] != -INFINITY) ? __builtin_amdgcn_exp2f(m[u] - Mb) : 0.f;
           L = fmaf(w, l[u], L);
           A = fmaf(w, a[u], A);
@@ -404,21 +405,23 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_kernel(
   }
 }
 
-// Splits per (request, kv-head).  With fewer than 256 pairs, about 256 workgroups,
-// each of at least 256 rows, and at most 8 splits: the merging split loads the
-// partials eight at a time, so a ninth costs it another memory round trip (on the
-// long-dialogue shape, 16 pairs of ~8k rows, 8 splits take 18.1 us per call, 16
-// take 19.3).  With 256 pairs or more, one split, or three when the longest context
-// reaches 2048 rows, so that the longest pairs do not outlast the rest of the call
-// when lengths are uneven (dynamic-budget batch: 1 split 127.7 us, 2 117.1, 3 111.4,
-// 4 121.3 per call).
+// Splits per (request, kv-head).  A workgroup fills a CU (one per CU), so with fewer
+// than 256 pairs the grid takes as many splits as keep every workgroup resident at
+// once (a 257th would wait for a whole workgroup to finish: on the 8B-shaped batch,
+// 64 pairs, 4 splits take 13.7 us per call and 5 take 18.3), each of at least 256
+// rows, and at most 16 (the merging split loads sixteen partials per memory round
+// trip; on the long-dialogue shape, 16 pairs of ~8k rows, 8 splits take 19.0 us per
+// call and 16 take 18.5, 22.6 against 24.6 us with the caches cold).  With 256 pairs
+// or more, one split, or three when the longest context reaches 2048 rows, so that
+// the longest pairs do not outlast the rest of the call when lengths are uneven
+// (dynamic-budget batch: 1 split 127.7 us, 2 117.1, 3 111.4, 4 121.3 per call).
 int decode_splits(int batch, int Hkv, int max_ctx) {
   const long pairs = static_cast<long>(batch) * Hkv;
   if (pairs >= 256) return max_ctx >= 2048 ? 3 : 1;
-  long s = (256 + pairs - 1) / pairs;
+  long s = 256 / pairs;
   const long by_rows = (static_cast<long>(max_ctx) + 255) / 256;
   if (s > by_rows) s = by_rows;
-  if (s > 8) s = 8;
+  if (s > kMergeBatch) s = kMergeBatch;
   return static_cast<int>(s < 1 ? 1 : s);
 }
 
