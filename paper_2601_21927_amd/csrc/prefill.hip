@@ -44,7 +44,32 @@ namespace sonic {
 // K-operand layout the P.V product needs.  The permutation is an involution.
 __device__ __forceinline__ int perm32(int m) { return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1); }
 
-__device__ __forceinline__ int acc_key(int v, int g) { return v < 8 ? 8 * g + v : 16 + 8 * g + (v - 8); }
+// Key of accumulator element v, less the lane half's 8g.  It is a compile-time
+// constant once the element loop is unrolled, so a bound compared with it is shifted
+// by 8g once, instead of 32 per-lane key indices being held in registers for the
+// whole kernel.
+__device__ __forceinline__ constexpr int acc_key0(int v) { return v < 8 ? v : 8 + v; }
+
+// Instruction order of one product block of NMFMA MFMAs whose operands each take
+// READS LDS reads: the reads of the first AHEAD products, then one MFMA and the reads
+// of one more product at a time, then the last AHEAD MFMAs.  The reads so run AHEAD
+// products ahead of the MFMA that consumes them, hiding the LDS latency behind the
+// matrix cores (the compiler, left alone, keeps one read ahead to save registers).
+// Placed after the block's code, in the same basic block.
+constexpr int kAheadS = 4;    // K-operand reads ahead of the S product's MFMAs
+constexpr int kAheadPV = 3;   // V-operand products read ahead in the P.V product
+
+template <int NMFMA, int READS, int AHEAD>
+__device__ __forceinline__ void order_reads_ahead() {
+  static_assert(AHEAD >= 1 && AHEAD <= NMFMA, "lookahead within the block");
+  __builtin_amdgcn_sched_group_barrier(0x100, READS * AHEAD, 0);   // DS reads
+#pragma unroll
+  for (int i = 0; i < NMFMA - AHEAD; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              // one MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, READS, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, AHEAD, 0);
+}
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) const void global_void_t;
@@ -308,6 +333,7 @@ __global__ __launch_bounds__(G * kWave * KS, 3 - KS) void prefill_kernel(AttnRow
           sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ds], sacc[kb], 0, 0, 0);
         }
       }
+      order_reads_ahead<2 * DS, 1, kAheadS>();
 
       wait_vm<2 * NJ>();
       lds_barrier();                                   // V(c) in LDS; every wave is past S(c)
@@ -317,12 +343,12 @@ __global__ __launch_bounds__(G * kWave * KS, 3 - KS) void prefill_kernel(AttnRow
         // Row n sees every key before the diagonal block and diagonal keys j <= n:
         // virtual key vk is visible iff vk < min(nv, nF + n + 1).  One compare and a
         // select per element, no divergent branches.
-        const int lim = min(nv, nF + n + 1) - vk0;
+        const int lim_g = min(nv, nF + n + 1) - vk0 - 8 * g;   // bound on acc_key0
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int e = 0; e < 16; ++e)
-            sacc[kb][e] = (kb * 32 + acc_key(e, g) < lim) ? sacc[kb][e] : -INFINITY;
+            sacc[kb][e] = (kb * 32 + acc_key0(e) < lim_g) ? sacc[kb][e] : -INFINITY;
       }
       float mloc = -INFINITY;
 #pragma unroll
@@ -346,6 +372,7 @@ __global__ __launch_bounds__(G * kWave * KS, 3 - KS) void prefill_kernel(AttnRow
       const int nx0 = max(nex_lo - vk0, 0), nx1 = min(npre - vk0, kKeyChunk);
       const bool nex_all = STATS && nx0 == 0 && nx1 == kKeyChunk;
       const bool nex_some = STATS && nx0 < nx1 && !nex_all;
+      const int nx0_g = nx0 - 8 * g, nx1_g = nx1 - 8 * g;   // the same range on acc_key0
       float lsum = 0.f, nsum = 0.f;
       bf16x8 pb[4];
 #pragma unroll
@@ -357,8 +384,8 @@ __global__ __launch_bounds__(G * kWave * KS, 3 - KS) void prefill_kernel(AttnRow
           hi[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][8 + e], scale_log2, -m_run));
           if (STATS) lsum += lo[e] + hi[e];
           if (nex_some) {
-            const int klo = kb * 32 + acc_key(e, g), khi = kb * 32 + acc_key(8 + e, g);
-            nsum += ((klo >= nx0 && klo < nx1) ? lo[e] : 0.f) + ((khi >= nx0 && khi < nx1) ? hi[e] : 0.f);
+            const int klo = kb * 32 + acc_key0(e), khi = kb * 32 + acc_key0(8 + e);
+            nsum += ((klo >= nx0_g && klo < nx1_g) ? lo[e] : 0.f) + ((khi >= nx0_g && khi < nx1_g) ? hi[e] : 0.f);
           }
         }
         pb[2 * kb] = __builtin_convertvector(lo, bf16x8);
@@ -394,6 +421,7 @@ __global__ __launch_bounds__(G * kWave * KS, 3 - KS) void prefill_kernel(AttnRow
                                                              0, 0);
         }
       }
+      order_reads_ahead<4 * DB, 2, kAheadPV>();
     };
 
     stage_k(c_first, kbuf0);
@@ -595,6 +623,7 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_pp_kernel(AttnRows rows,
                                                                0, 0);
           }
         }
+        order_reads_ahead<4 * DB, 2, kAheadPV>();
       }
       if (c < nch) {
 #pragma unroll
@@ -608,17 +637,18 @@ __global__ __launch_bounds__(G * kWave, 2) void prefill_pp_kernel(AttnRows rows,
             sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ds], sacc[kb], 0, 0, 0);
           }
         }
+        order_reads_ahead<2 * DS, 1, kAheadS>();
       }
     };
     // softmax phase c: mask, lazy max, P(c) in bf16 and the sum of its rounded values
     auto softmax_phase = [&](int c) {
       const int vk0 = c * kKeyChunk;
       if (vk0 + kKeyChunk > nF) {
-        const int lim = min(nv, nF + n + 1) - vk0;
+        const int lim_g = min(nv, nF + n + 1) - vk0 - 8 * g;   // bound on acc_key0
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) sacc[kb][e] = (kb * 32 + acc_key(e, g) < lim) ? sacc[kb][e] : -INFINITY;
+          for (int e = 0; e < 16; ++e) sacc[kb][e] = (kb * 32 + acc_key0(e) < lim_g) ? sacc[kb][e] : -INFINITY;
       }
       float mloc = -INFINITY;
 #pragma unroll
