@@ -220,4 +220,22 @@ constexpr int kScratchMaxPairs = 12288;
 constexpr size_t kScratchCounterBytes = (kScratchMaxRequests + kScratchMaxPairs) * sizeof(int32_t);   // 64 KiB
 constexpr size_t kScratchBytes = size_t(8) << 20;
 
+// Instruction order of one product block of NMFMA MFMAs whose operands each take
+// READS LDS reads: the reads of the first AHEAD products, then one MFMA and the reads
+// of one more product at a time, then the last AHEAD MFMAs.  The reads so run AHEAD
+// products ahead of the MFMA that consumes them, hiding the LDS latency behind the
+// matrix cores (the compiler, left alone, keeps one read ahead to save registers).
+// Placed after the block's code, in the same basic block.
+template <int NMFMA, int READS, int AHEAD>
+__device__ __forceinline__ void order_reads_ahead() {
+  static_assert(AHEAD >= 1 && AHEAD <= NMFMA, "lookahead within the block");
+  __builtin_amdgcn_sched_group_barrier(0x100, READS * AHEAD, 0);   // DS reads
+#pragma unroll
+  for (int i = 0; i < NMFMA - AHEAD; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              // one MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, READS, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, AHEAD, 0);
+}
+
 }  // namespace sonic

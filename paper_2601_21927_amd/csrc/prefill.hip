@@ -50,26 +50,11 @@ __device__ __forceinline__ int perm32(int m) { return (m & ~12) | ((m & 4) << 1)
 // whole kernel.
 __device__ __forceinline__ constexpr int acc_key0(int v) { return v < 8 ? v : 8 + v; }
 
-// Instruction order of one product block of NMFMA MFMAs whose operands each take
-// READS LDS reads: the reads of the first AHEAD products, then one MFMA and the reads
-// of one more product at a time, then the last AHEAD MFMAs.  The reads so run AHEAD
-// products ahead of the MFMA that consumes them, hiding the LDS latency behind the
-// matrix cores (the compiler, left alone, keeps one read ahead to save registers).
-// Placed after the block's code, in the same basic block.
-constexpr int kAheadS = 4;    // K-operand reads ahead of the S product's MFMAs
-constexpr int kAheadPV = 3;   // V-operand products read ahead in the P.V product
+// LDS reads run ahead of the MFMAs (order_reads_ahead): K-operand reads of the S
+// product, V-operand products of the P.V product
+constexpr int kAheadS = 4;
+constexpr int kAheadPV = 3;
 
-template <int NMFMA, int READS, int AHEAD>
-__device__ __forceinline__ void order_reads_ahead() {
-  static_assert(AHEAD >= 1 && AHEAD <= NMFMA, "lookahead within the block");
-  __builtin_amdgcn_sched_group_barrier(0x100, READS * AHEAD, 0);   // DS reads
-#pragma unroll
-  for (int i = 0; i < NMFMA - AHEAD; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              // one MFMA
-    __builtin_amdgcn_sched_group_barrier(0x100, READS, 0);
-  }
-  __builtin_amdgcn_sched_group_barrier(0x008, AHEAD, 0);
-}
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) const void global_void_t;

@@ -17,7 +17,8 @@
 // global memory into LDS (direct-to-LDS loads), double-buffered: step s + 1
 // streams in while step s is multiplied.  LDS rows are 128 bytes with an XOR
 // swizzle on the 16-byte chunk index, so the fragment reads (32 rows at one
-// chunk) are bank-conflict free.  Each fragment read feeds two MFMAs.
+// chunk) are bank-conflict free.  Each fragment read feeds two MFMAs, and the
+// reads are scheduled two K sub-steps ahead of the MFMAs that consume them.
 // Tiles are laid out so that the workgroups of one XCD share a band of output
 // columns and walk the row tiles in order: the x rows a tile needs are also
 // needed by the tiles of the other columns of the band, resident on the same
@@ -189,6 +190,8 @@ __global__ __launch_bounds__(kPThreads) void routed_gemm_kernel(
         for (int bj = 0; bj < kPBN; ++bj)
           acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[bi], bf[bj], acc[bi][bj], 0, 0, 0);
     }
+    // the fragment reads run two K sub-steps (eight reads) ahead of the MFMAs
+    order_reads_ahead<(kPK / 16) * kPBM * kPBN, 1, 2 * (kPBM + kPBN)>();
   };
 
   // double buffer: each wave issues IA + IB loads per step, so "step s has landed"
