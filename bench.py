@@ -27,7 +27,8 @@ times come from the timed steps themselves.  Attached:
 * cpu_baseline: the fp64 oracle on the host cores, on a bounded sample.
 
 --profile-pass runs only the headline path a few times, eagerly (for counter
-collection with rocprofv3).
+collection with rocprofv3); --calibration-copy MIB runs a plain copy of known size
+(the reference that scales the HBM byte counters).
 """
 from __future__ import annotations
 
@@ -72,6 +73,17 @@ def measured_traffic(key: str):
     return ent.get("bytes_per_launch")
 
 
+def measured_counters(key: str) -> dict:
+    """MFMA-busy fraction and tile efficiency (visible flops / flops of the executed MFMAs)
+    from the committed rocprofv3 counter runs, if they were taken on the current kernel
+    sources (else null)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    ent = json.load(open(path)).get(key) if os.path.exists(path) else None
+    if not ent or ent.get("source_hash") != kernel_source_hash():
+        return {"mfma_busy": None, "tile_efficiency": None}
+    return {"mfma_busy": ent.get("mfma_busy"), "tile_efficiency": ent.get("tile_efficiency")}
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -89,6 +101,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true", help="only the headline workload")
+    ap.add_argument("--calibration-copy", type=int, default=0, metavar="MIB",
+                    help="run a plain device copy of MIB MiB three times and exit (the known-size "
+                         "reference for the FETCH_SIZE / WRITE_SIZE counters)")
     ap.add_argument("--profile-pass", action="store_true",
                     help="run the headline path twice eagerly (prefill, compaction, decode loop) and exit")
     return ap.parse_args()
@@ -220,16 +235,22 @@ class Timer:
     def median(self, fn, n, pre=None):
         return float(np.median([self.once(fn, pre) for _ in range(n)]))
 
-    def cold(self, fn, pre=None, n=COLD_REPS):
-        """Single launches with the 256 MB Infinity Cache evicted: a 1 GiB write before each."""
+    def cold(self, fn, pre=None, n=COLD_REPS, clean=False):
+        """Single launches with the 256 MB Infinity Cache evicted: a 1 GiB write before each.
+        The write leaves the cache full of dirty lines, which the timed launch then writes
+        back as it misses; clean=True reads the 1 GiB once more after the write, so that
+        the launch finds clean lines to evict (reported beside, labelled)."""
         torch = self.torch
         if self.flush is None:
             self.flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+            self.flush_sum = torch.empty((), dtype=torch.float32, device="cuda")
         ts = []
         for i in range(n):
             if pre is not None:
                 pre()
             self.flush.fill_(float(i))
+            if clean:
+                torch.sum(self.flush, dim=0, out=self.flush_sum)
             ts.append(self.once(fn))
         return float(np.median(ts))
 
@@ -291,6 +312,16 @@ def headline(args, timer):
     pf_cold = timer.cold(P.prefill, n=3)
     cp_cold = timer.cold(P.compact)
     dc_cold = timer.cold(P.decode_one, pre=P.compact)   # from the freshly compacted cache
+    cp_clean = timer.cold(P.compact, clean=True)
+    dc_clean = timer.cold(P.decode_one, pre=P.compact, clean=True)
+    # reference: a plain device copy moving the same bytes as one decode call (half read,
+    # half written), under both cold protocols
+    dec1_bytes = float((P.kept + 1).sum()) * P.row_bytes * 2
+    cp_src = torch.empty(int(dec1_bytes) // 2, dtype=torch.uint8, device="cuda")
+    cp_dst = torch.empty_like(cp_src)
+    copy_cold = timer.cold(lambda: cp_dst.copy_(cp_src))
+    copy_clean = timer.cold(lambda: cp_dst.copy_(cp_src), clean=True)
+    del cp_src, cp_dst
     torch.cuda.synchronize()
     assert P.db.read_status() == 0
 
@@ -315,7 +346,6 @@ def headline(args, timer):
         torch.cuda.empty_cache()
 
     dec_bytes = P.decode_bytes(P.kept)
-    dec1_bytes = float((P.kept + 1).sum()) * P.row_bytes * 2
     cmp_bytes = P.compact_bytes()
     vf = P.visible_flops
     value = P.B * P.steps / (ms_per_step * 1e-3)
@@ -333,6 +363,14 @@ def headline(args, timer):
         "decode_frac_hbm_peak_warm": rnd(gbs(dec_bytes, dc_ms) / PEAK_HBM_GBS),
         "decode_us_one_call_cold": rnd(dc_cold * 1e3, 2), "decode_gbs_one_call_cold": rnd(gbs(dec1_bytes, dc_cold), 1),
         "decode_frac_hbm_peak_cold": rnd(gbs(dec1_bytes, dc_cold) / PEAK_HBM_GBS),
+        "compact_us_cold_clean": rnd(cp_clean * 1e3, 2),
+        "compact_frac_hbm_peak_cold_clean": rnd(gbs(cmp_bytes, cp_clean) / PEAK_HBM_GBS),
+        "decode_us_one_call_cold_clean": rnd(dc_clean * 1e3, 2),
+        "decode_frac_hbm_peak_cold_clean": rnd(gbs(dec1_bytes, dc_clean) / PEAK_HBM_GBS),
+        "copy_same_bytes_as_decode_call_us_cold": rnd(copy_cold * 1e3, 2),
+        "copy_same_bytes_as_decode_call_frac_hbm_peak_cold": rnd(gbs(dec1_bytes, copy_cold) / PEAK_HBM_GBS),
+        "copy_same_bytes_as_decode_call_us_cold_clean": rnd(copy_clean * 1e3, 2),
+        "copy_same_bytes_as_decode_call_frac_hbm_peak_cold_clean": rnd(gbs(dec1_bytes, copy_clean) / PEAK_HBM_GBS),
         "step_ms_event_median": rnd(step_ev),
     }
     for name, f in full.items():
@@ -349,11 +387,12 @@ def headline(args, timer):
         ach = vf / (pf_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": rnd(ach, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": rnd(ach / PEAK_BF16_TFLOPS), "traffic": measured_traffic(f"prefill_w{HEADLINE}"),
-                "kernel": "sonic_segment_attn_prefill: plan kernels + prefill_kernel<128, 7, false, 1>",
+                "kernel": "sonic_segment_attn_prefill: plan kernels + prefill_pp_kernel<128, 7>",
                 "per_launch": f"{vf:.6g} visible flops (4 d flops per visible (row, key, q-head))",
                 "timing": "HIP events around the prefill graph replay of each timed step (median)",
                 "cold_achieved": rnd(vf / (pf_cold * 1e-3) / 1e12, 2),
                 "cold_frac": rnd(vf / (pf_cold * 1e-3) / 1e12 / PEAK_BF16_TFLOPS)}
+        roof.update(measured_counters(f"prefill_w{HEADLINE}"))
     elif dominant == "decode":
         ach = gbs(dec1_bytes, dc_cold)
         roof = {"bound": "hbm", "achieved": rnd(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -620,6 +659,16 @@ def main():
     sonic.lib()
     torch.cuda.set_device(0)
     timer = Timer(torch)
+
+    if args.calibration_copy > 0:
+        src = torch.empty(args.calibration_copy << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration_copy_bytes": src.numel()}))
+        return
 
     if args.profile_pass:
         P = Path(HEADLINE, "cuda:0")
