@@ -16,52 +16,101 @@
 // the tail rows after the body (staged in the workspace beforehand, the regions
 // may overlap) follow them.
 #include "common.h"
+#include "scan.h"
 
 namespace sonic {
 
 constexpr int kExtendThreads = 256;
 
-// One workgroup per request: check the lengths, then one descriptor per block of
-// up to 32 new Nexus rows.  ReqInfo.nruns carries the number of tail rows after
-// the body to the cache update.
+// Lengths of request j, checked: its new-row count kn, the tail rows after its
+// segment's body (rest), its block count and cost (every block costs the same:
+// all keep + body + kn keys).  Returns 0, SONIC_ERR_BAD_LAYOUT or SONIC_ERR_CAPACITY.
+struct ExtendReq {
+  int kn, rest, nt;
+  int64_t cost;
+};
+__device__ __forceinline__ int extend_check(int j, const int32_t *__restrict__ nexus_cu,
+                                            const int32_t *__restrict__ keep_len, const int32_t *__restrict__ body_len,
+                                            const int32_t *__restrict__ cache_len, const int32_t *__restrict__ row_cap,
+                                            int max_rows, int total_new, ExtendReq *r) {
+  const int s = nexus_cu[j];
+  const int e = nexus_cu[j + 1];
+  const int len = cache_len[j];
+  const int keep = keep_len[j];
+  const int cap = row_cap[j];
+  const int body = body_len != nullptr ? body_len[j] : len - keep;
+  const bool bad = s < 0 || e < s || e > total_new || keep < 0 || keep > len || len > cap || len > max_rows ||
+                   body < 0 || body > len - keep;
+  *r = ExtendReq{0, 0, 0, 0};
+  if (bad) return SONIC_ERR_BAD_LAYOUT;
+  const int kn = e - s;
+  const int rest = len - keep - body;
+  if (keep + kn + rest > cap) return SONIC_ERR_CAPACITY;
+  const int nt = (kn + kTileRows - 1) / kTileRows;
+  *r = ExtendReq{kn, rest, nt, static_cast<int64_t>(nt) * ((keep + body + kn + kKeyChunk - 1) / kKeyChunk)};
+  return 0;
+}
+
+// One workgroup per request b, the whole plan in one launch.  The lengths of every
+// request are inputs, so each workgroup checks all of them and knows the batch's
+// block counts and costs: blocks run requests by decreasing cost (ties by index),
+// and request b's first slot in the work order is the number of blocks of the
+// requests ranked before it.  A bad request, or an error left on the status word by
+// an earlier call, makes the whole call write nothing (no work items).  Then one
+// descriptor per block of up to 32 new Nexus rows; ReqInfo.nruns carries the
+// number of tail rows after the body to the cache update.
 __global__ __launch_bounds__(kExtendThreads) void plan_extend_kernel(
-    const int32_t *__restrict__ nexus_cu, const int32_t *__restrict__ keep_len, const int32_t *__restrict__ body_len,
-    const int32_t *__restrict__ cache_len, const int32_t *__restrict__ row_cap, int max_rows, int total_new,
-    PrefillWs ws, int32_t *status) {
+    int batch, const int32_t *__restrict__ nexus_cu, const int32_t *__restrict__ keep_len,
+    const int32_t *__restrict__ body_len, const int32_t *__restrict__ cache_len, const int32_t *__restrict__ row_cap,
+    int max_rows, int total_new, PrefillWs ws, int32_t *status) {
+  __shared__ int lds[kExtendThreads / kWave + 1];
+  __shared__ int s_ok;
   const int b = blockIdx.x;
-  const int s = nexus_cu[b];
-  const int e = nexus_cu[b + 1];
-  const int len = cache_len[b];
-  const int keep = keep_len[b];
-  const int cap = row_cap[b];
-  const int body = body_len != nullptr ? body_len[b] : len - keep;
-  bool bad = s < 0 || e < s || e > total_new || keep < 0 || keep > len || len > cap || len > max_rows;
-  bad = bad || body < 0 || body > len - keep;
-  const int kn = bad ? 0 : e - s;
-  const int rest = bad ? 0 : len - keep - body;
-  if (bad || keep + kn + rest > cap) {
+  if (b == 0 && threadIdx.x < kNumXcd) ws.ctrl[8 + threadIdx.x] = 0;   // the work queues
+  const bool clear = block_status_clear(status, &s_ok);
+  ExtendReq own;
+  const int own_code = extend_check(b, nexus_cu, keep_len, body_len, cache_len, row_cap, max_rows, total_new, &own);
+  int before = 0, all = 0, nbad = 0;
+  for (int j0 = 0; j0 < batch; j0 += kExtendThreads) {
+    const int j = j0 + threadIdx.x;
+    ExtendReq r{0, 0, 0, 0};
+    int code = 0;
+    if (j < batch) code = extend_check(j, nexus_cu, keep_len, body_len, cache_len, row_cap, max_rows, total_new, &r);
+    const int nb = (r.cost > own.cost || (r.cost == own.cost && j < b)) ? r.nt : 0;
+    int t0, t1, t2;
+    block_int_scan<kExtendThreads>(nb, &t0, lds);
+    block_int_scan<kExtendThreads>(r.nt, &t1, lds);
+    block_int_scan<kExtendThreads>(code != 0 ? 1 : 0, &t2, lds);
+    before += t0;
+    all += t1;
+    nbad += t2;
+  }
+  if (own_code != 0 && clear && threadIdx.x == 0) raise_status(status, own_code);
+  if (!clear || nbad > 0) {
     if (threadIdx.x == 0) {
-      raise_status(status, bad ? SONIC_ERR_BAD_LAYOUT : SONIC_ERR_CAPACITY);
+      if (b == 0) ws.ctrl[0] = 0;
       ws.req[b] = ReqInfo{0, 0, 0, 0, 0, 0};
     }
     return;
   }
-  const int nt = (kn + kTileRows - 1) / kTileRows;
-  for (int j = threadIdx.x; j < nt; j += kExtendThreads) {
+  if (b == 0 && threadIdx.x == 0) ws.ctrl[0] = all;
+  const int s = nexus_cu[b];
+  const int keep = keep_len[b];
+  const int body = cache_len[b] - keep - own.rest;
+  for (int j = threadIdx.x; j < own.nt; j += kExtendThreads) {
     TileDesc d;
     d.req = b;
     d.p0 = j * kTileRows;
-    d.nrows = min(kTileRows, kn - d.p0);
+    d.nrows = min(kTileRows, own.kn - d.p0);
     d.npre = keep + body;  // the kept cache rows and the segment's body
     d.seg_start = 0;       // then every new Nexus row, no causal part
-    d.seg_len = kn;
+    d.seg_len = own.kn;
     d.ndiag = 0;
     d.pad = 0;
     ws.tiles[s + j] = d;
+    ws.order[before + j] = s + j;   // a request's blocks all cost the same: index order
   }
-  // every block of the request costs the same: all keep + body + kn keys
-  const int64_t cost = static_cast<int64_t>(nt) * ((keep + body + kn + kKeyChunk - 1) / kKeyChunk);
-  if (threadIdx.x == 0) ws.req[b] = ReqInfo{nt, 0, kn, rest, cost, 0};
+  if (threadIdx.x == 0) ws.req[b] = ReqInfo{own.nt, 0, own.kn, own.rest, own.cost, 0};
 }
 
 // Before the cache update: the tail rows after the body, rows keep + body .. len of
@@ -120,16 +169,12 @@ __global__ __launch_bounds__(kExtendThreads) void extend_append_kernel(
   if (blockIdx.x == 0 && threadIdx.x == 0) cache_len[b] = keep + kn + rest;   // nothing else reads it here
 }
 
-hipError_t launch_plan_order(int batch, const int32_t *cu, PrefillWs ws, int32_t *status, hipStream_t stream);
-
 hipError_t launch_plan_extend(int batch, int total_new, int max_rows, const int32_t *nexus_cu,
                               const int32_t *keep_len, const int32_t *body_len, const int32_t *cache_len,
                               const int32_t *row_cap, PrefillWs ws, int32_t *status, hipStream_t stream) {
-  plan_extend_kernel<<<dim3(batch), dim3(kExtendThreads), 0, stream>>>(nexus_cu, keep_len, body_len, cache_len,
+  plan_extend_kernel<<<dim3(batch), dim3(kExtendThreads), 0, stream>>>(batch, nexus_cu, keep_len, body_len, cache_len,
                                                                         row_cap, max_rows, total_new, ws, status);
-  const hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  return launch_plan_order(batch, nexus_cu, ws, status, stream);
+  return hipGetLastError();
 }
 
 static unsigned extend_chunks(long rows, int row_pieces) {
