@@ -314,3 +314,20 @@ def test_extend_body_longer_than_the_tail_is_a_layout_error():
     assert int(case.status.item()) == sonic.ERR_BAD_LAYOUT
     assert np.array_equal(bf16_to_host(case.kc), kc0) and np.array_equal(case.length.cpu().numpy(), len0)
     assert torch.all(case.out == 7.0)
+
+
+def test_extend_with_a_pending_layout_error_writes_nothing():
+    """A layout error left on the status word by an earlier call stops the whole step: no output,
+    no cache row or length changes, and the status keeps the earlier error."""
+    H.need_gpu()
+    rng = np.random.default_rng(43)
+    lays = _ending_layouts(rng, 3, max_h=3, max_b=40, max_k=12, max_s=20)
+    batch = W.make_batch("pending", lays, 4, 2, 64, seed=43)
+    case = ExtendCase(batch)
+    case.status.fill_(sonic.ERR_BAD_LAYOUT)
+    kc0, vc0, len0 = bf16_to_host(case.kc).copy(), bf16_to_host(case.vc).copy(), case.length.cpu().numpy().copy()
+    assert case.run() == sonic.OK
+    assert int(case.status.item()) == sonic.ERR_BAD_LAYOUT
+    assert np.array_equal(bf16_to_host(case.kc), kc0) and np.array_equal(bf16_to_host(case.vc), vc0)
+    assert np.array_equal(case.length.cpu().numpy(), len0)
+    assert torch.all(case.out == 7.0)
