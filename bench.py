@@ -15,12 +15,16 @@ compaction).  A step is three HIP graph replays (prefill, compaction, the 512
 decode calls) with HIP events between them on the launch stream, so the phase
 times come from the timed steps themselves.  Attached:
 
-* phases of the step, the back-to-back and cold-cache (1 GiB write before a
-  single launch) rates of each kernel, and the same 512-step decode over the
-  full, uncompressed context in two forms: the text-only cache (what a model
-  without Nexus tokens keeps) and the augmented cache with the hierarchical
-  mask applied per row;
-* the roofline of the kernel that dominates the step;
+* phases of the step, the back-to-back and cold-cache rates of each kernel
+  (a 1 GiB write before a single launch; "clean" cold also reads the 1 GiB
+  back, so that the launch evicts clean lines), a plain copy of one decode
+  call's bytes under both cold protocols for reference, and the same 512-step
+  decode over the full, uncompressed context in two forms: the text-only cache
+  (what a model without Nexus tokens keeps) and the augmented cache with the
+  hierarchical mask applied per row;
+* the roofline of the kernel that dominates the step, with the HBM traffic,
+  MFMA-busy fraction and tile efficiency of the committed counter runs when they
+  were taken on the current kernel sources;
 * other_workloads: the 8B-shaped workload's whole step, the ragged workload's
   prefill and decode, the dynamic-budget workload's 1024-step decode against
   its uncompressed caches, and the four widened rows on the 8B shape;
