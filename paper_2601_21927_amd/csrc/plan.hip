@@ -340,8 +340,8 @@ __global__ __launch_bounds__(kGatherThreads) void gather_prefix_kernel(const int
   }
 }
 
-// Work order of the descriptors of a batch (request b's at offset cu[b] of ws.tiles)
-// and reset queues; shared by the prefill and the next-turn Nexus step.
+// Work order of the prefill's descriptors (request b's at offset cu[b] of ws.tiles)
+// and reset queues.
 hipError_t launch_plan_order(int batch, const int32_t *cu, PrefillWs ws, int32_t *status, hipStream_t stream) {
   plan_order_kernel<<<dim3(batch), dim3(kPlanThreads), 0, stream>>>(batch, cu, ws, status);
   return hipGetLastError();
